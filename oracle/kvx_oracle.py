@@ -1,0 +1,182 @@
+"""CPU oracle for the paged KV-cache gather / scatter / transfer path.
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and
+the CPU-baseline leg of ``bench.py`` may import this module; the product path
+(the HIP library and its binding) never does.
+
+The arithmetic lives in ``kvx_oracle.c`` (plain C, one element at a time, in
+the order request -> token -> layer -> kv -> head -> dim).  This module only
+compiles it with gcc, loads it with ctypes and marshals numpy arrays.  What it
+computes is stated in the C file's header: Omni-Flow Sec. 4.1.1 (layer x page
+x slice addressing), Sec. 4.1.2 (conversion between the paged layout and the
+flat serialization), Sec. 4.1.4 (partial pages keep their other slots) and
+Sec. 5.2 (slot-to-page translation through a page table).
+
+Inputs are duck-typed: a pool shape is any object with integer attributes
+``L C H D T N e`` and a ``layout`` name (``"LPCTHD"``, ``"LPCHTD"``,
+``"PLCTHD"`` or ``"PLCHTD"``); a buffer shape has ``L C H D e`` and ``cap``
+(elements).  Request records are an ``(n, 6)`` int64 array with columns
+``src_pt_off, dst_pt_off, buf_off, src_start, dst_start, n_tokens``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+SOURCE = os.path.join(HERE, "kvx_oracle.c")
+LIBRARY = os.path.join(HERE, "libkvx_oracle.so")
+
+LAYOUT_CODES = {"LPCTHD": 0, "LPCHTD": 1, "PLCTHD": 2, "PLCHTD": 3}
+
+ERR_SRC_PAGE = 1
+ERR_DST_PAGE = 2
+ERR_PT_RANGE = 4
+ERR_BAD_REQ = 8
+
+
+class _Pool(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int64) for k in ("L", "C", "H", "D", "T", "N", "e", "layout")]
+
+
+class _Buf(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int64) for k in ("L", "C", "H", "D", "e", "cap")]
+
+
+def build(source: str = SOURCE, output: str = LIBRARY) -> str:
+    """Compile the oracle with gcc (plain -O2, no vector intrinsics)."""
+    cmd = ["gcc", "-O2", "-std=c99", "-Wall", "-Werror", "-shared", "-fPIC",
+           "-o", output, source]
+    subprocess.run(cmd, check=True)
+    return output
+
+
+def pool_elems(p) -> int:
+    return p.L * p.C * p.H * p.D * p.T * p.N
+
+
+def _pool(p) -> _Pool:
+    if p.layout not in LAYOUT_CODES:
+        raise ValueError(f"unknown layout {p.layout!r}")
+    return _Pool(p.L, p.C, p.H, p.D, p.T, p.N, p.e, LAYOUT_CODES[p.layout])
+
+
+def _buf(b) -> _Buf:
+    return _Buf(b.L, b.C, b.H, b.D, b.e, b.cap)
+
+
+def _bytes(a: np.ndarray, nbytes: int, name: str, writable: bool = False) -> np.ndarray:
+    if not (isinstance(a, np.ndarray) and a.flags.c_contiguous):
+        raise TypeError(f"{name} must be a C-contiguous numpy array")
+    if writable and not a.flags.writeable:
+        raise ValueError(f"{name} must be writable")
+    if a.nbytes != nbytes:
+        raise ValueError(f"{name} holds {a.nbytes} bytes, expected {nbytes}")
+    return a
+
+
+def _i32(a) -> np.ndarray:
+    a = np.ascontiguousarray(a, dtype=np.int32)
+    return a if a.size else np.zeros(1, np.int32)
+
+
+def _reqs(a) -> tuple[np.ndarray, int]:
+    a = np.ascontiguousarray(a, dtype=np.int64).reshape(-1, 6)
+    return (a if len(a) else np.zeros((1, 6), np.int64)), len(a)
+
+
+def _same_elements(a, b):
+    for k in ("L", "C", "H", "D", "e"):
+        if getattr(a, k) != getattr(b, k):
+            raise ValueError(f"element shapes differ in {k}: {getattr(a, k)} vs {getattr(b, k)}")
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+class Oracle:
+    """One loaded copy of the oracle library (the tests load planted-mistake
+    builds of the same source through this class too)."""
+
+    def __init__(self, path: str = LIBRARY):
+        if not os.path.exists(path):
+            raise FileNotFoundError(f"{path} is not built; call oracle.kvx_oracle.build()")
+        lib = ctypes.CDLL(path)
+        vp, i64, u32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint32
+        pp, bp = ctypes.POINTER(_Pool), ctypes.POINTER(_Buf)
+        lib.ora_transfer.argtypes = [vp, pp, vp, pp, vp, i64, vp, i64, vp, i64]
+        lib.ora_transfer.restype = u32
+        lib.ora_gather.argtypes = [vp, pp, vp, bp, vp, i64, vp, i64]
+        lib.ora_gather.restype = u32
+        lib.ora_scatter.argtypes = [vp, bp, vp, pp, vp, i64, vp, i64]
+        lib.ora_scatter.restype = u32
+        self.lib = lib
+
+    def transfer(self, src: np.ndarray, src_shape, dst: np.ndarray, dst_shape,
+                 src_pt, dst_pt, reqs) -> int:
+        """Pool -> pool.  ``dst`` is updated in place; returns the error bits."""
+        _same_elements(src_shape, dst_shape)
+        _bytes(src, pool_elems(src_shape) * src_shape.e, "src")
+        _bytes(dst, pool_elems(dst_shape) * dst_shape.e, "dst", writable=True)
+        sp, dp = _i32(src_pt), _i32(dst_pt)
+        rq, nr = _reqs(reqs)
+        S, D = _pool(src_shape), _pool(dst_shape)
+        return int(self.lib.ora_transfer(
+            _ptr(src), ctypes.byref(S), _ptr(dst), ctypes.byref(D),
+            _ptr(sp), np.asarray(src_pt).size, _ptr(dp), np.asarray(dst_pt).size,
+            _ptr(rq), nr))
+
+    def gather(self, src: np.ndarray, src_shape, dst: np.ndarray, buf_shape,
+               src_pt, reqs) -> int:
+        """Pool -> flat buffer.  ``dst`` is updated in place."""
+        _same_elements(src_shape, buf_shape)
+        _bytes(src, pool_elems(src_shape) * src_shape.e, "src")
+        _bytes(dst, buf_shape.cap * buf_shape.e, "dst", writable=True)
+        sp = _i32(src_pt)
+        rq, nr = _reqs(reqs)
+        S, B = _pool(src_shape), _buf(buf_shape)
+        return int(self.lib.ora_gather(
+            _ptr(src), ctypes.byref(S), _ptr(dst), ctypes.byref(B),
+            _ptr(sp), np.asarray(src_pt).size, _ptr(rq), nr))
+
+    def scatter(self, src: np.ndarray, buf_shape, dst: np.ndarray, dst_shape,
+                dst_pt, reqs) -> int:
+        """Flat buffer -> pool.  ``dst`` is updated in place."""
+        _same_elements(buf_shape, dst_shape)
+        _bytes(src, buf_shape.cap * buf_shape.e, "src")
+        _bytes(dst, pool_elems(dst_shape) * dst_shape.e, "dst", writable=True)
+        dp = _i32(dst_pt)
+        rq, nr = _reqs(reqs)
+        B, D = _buf(buf_shape), _pool(dst_shape)
+        return int(self.lib.ora_scatter(
+            _ptr(src), ctypes.byref(B), _ptr(dst), ctypes.byref(D),
+            _ptr(dp), np.asarray(dst_pt).size, _ptr(rq), nr))
+
+
+_DEFAULT: Oracle | None = None
+
+
+def default() -> Oracle:
+    """The oracle built from ``kvx_oracle.c``; compiled on first use if absent."""
+    global _DEFAULT
+    if _DEFAULT is None:
+        if not os.path.exists(LIBRARY):
+            build()
+        _DEFAULT = Oracle(LIBRARY)
+    return _DEFAULT
+
+
+def transfer(*a, **k) -> int:
+    return default().transfer(*a, **k)
+
+
+def gather(*a, **k) -> int:
+    return default().gather(*a, **k)
+
+
+def scatter(*a, **k) -> int:
+    return default().scatter(*a, **k)

@@ -1,0 +1,327 @@
+"""Seeded synthetic workloads for the paged KV-cache transfer path.
+
+This module only *generates inputs*: pool and buffer shapes, request lengths,
+page tables, request records, source values and destination prefill
+patterns.  It holds none of the copy's arithmetic, and both the CPU oracle
+(through the tests) and the HIP path consume what it produces.
+
+Five workloads follow the shapes of the KV-cache movements Omni-Flow's Data
+Flow layer performs (Sec. 4.1: role-to-role handoff through the Global Params
+Pool, relayout between roles with different page sizes and layouts,
+partial-prefix reuse as in Sec. 5.1's incremental matching, and L1 GPU <->
+L2 CPU tier migration, Sec. 4.1.2):
+
+  1. tiny gather-then-scatter (2 layers, 16-token pages -> flat -> 32-token pages)
+  2. LLM role handoff (36 layers x 8 KV heads x 128, 64-token pages, 32 requests)
+  3. heterogeneous relayout (28 x 4 x 128, 16-token LPCTHD -> 64-token PLCHTD)
+  4. MLA latent cache (61 layers x 576, 64-token pages, copy of [p, len))
+  5. host-tier offload then onload of a 16 GiB page subset (config-2 shape)
+
+Each has a ``small`` variant with the same layouts, page sizes and row widths
+but fewer layers, heads, pages and tokens, for parity checks the oracle
+finishes in seconds.
+
+Request records are ``(n, 6)`` int64 arrays with columns
+``src_pt_off, dst_pt_off, buf_off, src_start, dst_start, n_tokens``.
+"""
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass, field
+
+import numpy as np
+
+LAYOUTS = ("LPCTHD", "LPCHTD", "PLCTHD", "PLCHTD")
+REQ_COLUMNS = ("src_pt_off", "dst_pt_off", "buf_off", "src_start", "dst_start", "n_tokens")
+
+
+@dataclass(frozen=True)
+class PoolSpec:
+    """A paged pool: L layers, C kv components (2 = K and V, 1 = MLA latent),
+    H heads, D head_dim, T tokens per page, N pages, e bytes per element."""
+    L: int
+    C: int
+    H: int
+    D: int
+    T: int
+    N: int
+    e: int = 2
+    layout: str = "LPCTHD"
+
+    @property
+    def elems(self) -> int:
+        return self.L * self.C * self.H * self.D * self.T * self.N
+
+    @property
+    def nbytes(self) -> int:
+        return self.elems * self.e
+
+    @property
+    def token_bytes(self) -> int:
+        """Bytes one token position occupies across all layers."""
+        return self.L * self.C * self.H * self.D * self.e
+
+
+@dataclass(frozen=True)
+class BufSpec:
+    """A flat buffer of per-request blocks [layer][kv][token][head][dim];
+    ``cap`` is its size in elements."""
+    L: int
+    C: int
+    H: int
+    D: int
+    e: int
+    cap: int
+
+    @property
+    def nbytes(self) -> int:
+        return self.cap * self.e
+
+    @property
+    def token_bytes(self) -> int:
+        return self.L * self.C * self.H * self.D * self.e
+
+
+@dataclass
+class Step:
+    op: str                      # "transfer" | "gather" | "scatter"
+    src: str                     # name of the side read
+    dst: str                     # name of the side written
+    src_pt: np.ndarray | None    # int32 page table of a pool source
+    dst_pt: np.ndarray | None    # int32 page table of a pool destination
+    reqs: np.ndarray             # (n, 6) int64 request records
+
+    @property
+    def n_tokens(self) -> int:
+        return int(self.reqs[:, 5].sum()) if len(self.reqs) else 0
+
+
+@dataclass
+class Workload:
+    key: int
+    title: str
+    sides: dict                  # name -> PoolSpec | BufSpec
+    steps: list
+    value_seed: int
+    prefill_tag: int
+    host_sides: tuple = ()       # sides that live in pinned host memory
+    notes: dict = field(default_factory=dict)
+
+    def algorithmic_bytes(self, step: Step) -> int:
+        """Payload read plus payload written by one step: every copied token
+        position moves token_bytes once in and once out."""
+        return 2 * step.n_tokens * self.sides[step.src].token_bytes
+
+
+def _ceil_div(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+def _reqs(rows) -> np.ndarray:
+    a = np.asarray(rows, dtype=np.int64).reshape(-1, 6)
+    return a
+
+
+def _take_pages(perm: np.ndarray, counts) -> tuple[np.ndarray, list]:
+    """Give request r the next counts[r] entries of a page permutation."""
+    offs, pos = [], 0
+    for c in counts:
+        offs.append(pos)
+        pos += int(c)
+    if pos > len(perm):
+        raise ValueError(f"workload needs {pos} pages, pool has {len(perm)}")
+    return perm[:pos].astype(np.int32), offs
+
+
+# --------------------------------------------------------------------------
+# the five workloads
+# --------------------------------------------------------------------------
+
+def config1() -> Workload:
+    """2 layers, 2 KV heads, head_dim 64; a 100-token request on 7 random
+    pages of a 64 x 16-token pool is gathered to a flat buffer, which is then
+    scattered into a 32 x 32-token pool on 4 random pages."""
+    rng = np.random.default_rng(1001)
+    L, C, H, D, e = 2, 2, 2, 64, 2
+    n = 100
+    src = PoolSpec(L, C, H, D, T=16, N=64, e=e, layout="LPCTHD")
+    dst = PoolSpec(L, C, H, D, T=32, N=32, e=e, layout="LPCTHD")
+    buf = BufSpec(L, C, H, D, e, cap=L * C * n * H * D)
+    src_pt = rng.permutation(src.N)[: _ceil_div(n, src.T)].astype(np.int32)
+    dst_pt = rng.permutation(dst.N)[: _ceil_div(n, dst.T)].astype(np.int32)
+    gather = Step("gather", "A", "buf", src_pt, None, _reqs([0, 0, 0, 0, 0, n]))
+    scatter = Step("scatter", "buf", "B", None, dst_pt, _reqs([0, 0, 0, 0, 0, n]))
+    return Workload(1, "tiny gather->flat->scatter, 2L x 2H x 64, 16->32-token pages",
+                    {"A": src, "buf": buf, "B": dst}, [gather, scatter],
+                    value_seed=2001, prefill_tag=1)
+
+
+def _transfer_workload(key, title, src: PoolSpec, dst: PoolSpec, lengths, starts,
+                       rng, notes=None) -> Workload:
+    """Requests hold positions [0, len); the copy moves [start, len) to the
+    same positions.  Each side draws one permutation of its pages and gives
+    request r the next ceil(len / T) of them."""
+    lengths = [int(x) for x in lengths]
+    starts = [int(x) for x in starts]
+    src_perm = rng.permutation(src.N)
+    dst_perm = rng.permutation(dst.N)
+    src_pt, src_off = _take_pages(src_perm, [_ceil_div(n, src.T) for n in lengths])
+    dst_pt, dst_off = _take_pages(dst_perm, [_ceil_div(n, dst.T) for n in lengths])
+    rows = [[so, do, 0, p, p, n - p] for so, do, p, n in zip(src_off, dst_off, starts, lengths)]
+    step = Step("transfer", "A", "B", src_pt, dst_pt, _reqs(rows))
+    wl = Workload(key, title, {"A": src, "B": dst}, [step],
+                  value_seed=2000 + key, prefill_tag=key, notes=notes or {})
+    wl.notes.setdefault("lengths", lengths)
+    wl.notes.setdefault("starts", starts)
+    return wl
+
+
+def config2(small: bool = False) -> Workload:
+    """LLM role handoff: 36 layers, 8 KV heads, head_dim 128, 4096 x 64-token
+    pools on both sides, 32 requests with lengths uniform in [1024, 8192]."""
+    if small:
+        rng = np.random.default_rng(1102)
+        L, H, N, nreq, lo, hi = 3, 2, 64, 4, 1, 700
+    else:
+        rng = np.random.default_rng(1002)
+        L, H, N, nreq, lo, hi = 36, 8, 4096, 32, 1024, 8192
+    pool = PoolSpec(L, 2, H, 128, T=64, N=N, e=2, layout="LPCTHD")
+    lengths = rng.integers(lo, hi + 1, size=nreq)
+    return _transfer_workload(2, f"LLM role handoff {L}L x {H}H x 128, 64-token pages, "
+                              f"{nreq} requests", pool, pool, lengths, [0] * nreq, rng)
+
+
+def config3(small: bool = False) -> Workload:
+    """Heterogeneous-role relayout: 28 layers, 4 KV heads, head_dim 128;
+    16-token LPCTHD pages into 64-token PLCHTD pages; 16 requests with
+    lengths uniform in [2048, 16384]."""
+    if small:
+        rng = np.random.default_rng(1103)
+        L, Ns, Nd, nreq, lo, hi = 3, 256, 64, 3, 50, 1000
+    else:
+        rng = np.random.default_rng(1003)
+        L, Ns, Nd, nreq, lo, hi = 28, 16384, 4096, 16, 2048, 16384
+    src = PoolSpec(L, 2, 4, 128, T=16, N=Ns, e=2, layout="LPCTHD")
+    dst = PoolSpec(L, 2, 4, 128, T=64, N=Nd, e=2, layout="PLCHTD")
+    lengths = rng.integers(lo, hi + 1, size=nreq)
+    return _transfer_workload(3, f"relayout {L}L x 4H x 128, 16-token LPCTHD -> 64-token "
+                              f"PLCHTD, {nreq} requests", src, dst, lengths, [0] * nreq, rng)
+
+
+def config4(small: bool = False) -> Workload:
+    """MLA-style compressed KV: 61 layers, one 576-wide latent (C = 1, H = 1),
+    64-token pages; 64 requests with lengths uniform in [4096, 32768]; only
+    positions [p, len) are copied, p uniform in [0, len/2)."""
+    if small:
+        rng = np.random.default_rng(1104)
+        L, nreq, lo, hi, align = 3, 4, 64, 1000, 16
+    else:
+        rng = np.random.default_rng(1004)
+        L, nreq, lo, hi, align = 61, 64, 4096, 32768, 256
+    lengths = rng.integers(lo, hi + 1, size=nreq)
+    starts = [int(rng.integers(0, n // 2)) for n in lengths]
+    pages = sum(_ceil_div(int(n), 64) for n in lengths)
+    N = _ceil_div(pages, align) * align
+    pool = PoolSpec(L, 1, 1, 576, T=64, N=N, e=2, layout="LPCTHD")
+    return _transfer_workload(4, f"MLA latent {L}L x 576, 64-token pages, {nreq} requests, "
+                              f"partial prefix [p, len)", pool, pool, lengths, starts, rng)
+
+
+def config5(small: bool = False) -> Workload:
+    """Host-tier offload/onload: the config-2 pool; a 16 GiB subset of random
+    pages (1820 pages = 28 requests x 65 full pages) is gathered into a
+    pinned host buffer [request][layer][kv][token][head][dim] and scattered
+    back into a fresh random sample of pool pages."""
+    if small:
+        rng = np.random.default_rng(1105)
+        L, H, N, nreq, per = 3, 2, 64, 3, 4
+    else:
+        rng = np.random.default_rng(1005)
+        L, H, N, nreq, per = 36, 8, 4096, 28, 65
+    pool = PoolSpec(L, 2, H, 128, T=64, N=N, e=2, layout="LPCTHD")
+    n = per * pool.T
+    block = L * 2 * n * H * 128
+    buf = BufSpec(L, 2, H, 128, 2, cap=nreq * block)
+    out_pages = rng.choice(N, size=nreq * per, replace=False).astype(np.int32)
+    in_pages = rng.choice(N, size=nreq * per, replace=False).astype(np.int32)
+    g_rows = [[r * per, 0, r * block, 0, 0, n] for r in range(nreq)]
+    s_rows = [[0, r * per, r * block, 0, 0, n] for r in range(nreq)]
+    steps = [Step("gather", "A", "buf", out_pages, None, _reqs(g_rows)),
+             Step("scatter", "buf", "A", None, in_pages, _reqs(s_rows))]
+    return Workload(5, f"host-tier offload/onload {L}L x {H}H x 128, {nreq * per} pages "
+                    f"({nreq} x {per})", {"A": pool, "buf": buf}, steps,
+                    value_seed=2005, prefill_tag=5, host_sides=("buf",))
+
+
+def config(k: int, small: bool = False) -> Workload:
+    if k == 1:
+        return config1()
+    return {2: config2, 3: config3, 4: config4, 5: config5}[k](small=small)
+
+
+def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:
+    return dataclasses.replace(spec, **kw)
+
+
+# --------------------------------------------------------------------------
+# values
+# --------------------------------------------------------------------------
+
+def normal_bf16_bytes(nbytes: int, seed: int) -> np.ndarray:
+    """N(0,1) samples rounded to bf16 (nearest-even), as raw bytes (CPU)."""
+    if nbytes % 2:
+        raise ValueError("bf16 data needs an even byte count")
+    x = np.random.default_rng(seed).standard_normal(nbytes // 2, dtype=np.float32)
+    b = x.view(np.uint32).astype(np.uint64)
+    b = (b + 0x7FFF + ((b >> 16) & 1)) >> 16
+    return b.astype(np.uint16).view(np.uint8)
+
+
+def random_bytes(nbytes: int, seed: int) -> np.ndarray:
+    return np.random.default_rng(seed).integers(0, 256, size=nbytes, dtype=np.uint8)
+
+
+def prefill_bytes(nbytes: int, tag: int, start_byte: int = 0) -> np.ndarray:
+    """Offset-coded destination prefill (CPU): the 8-byte group at byte
+    offset 8g holds the little-endian word 0x5A<<56 | tag<<48 | g, so any
+    byte can be regenerated from its offset."""
+    if nbytes % 8 or start_byte % 8:
+        raise ValueError("prefill covers whole 8-byte groups")
+    g = np.arange(start_byte // 8, (start_byte + nbytes) // 8, dtype=np.uint64)
+    w = (np.uint64(0x5A) << np.uint64(56)) | (np.uint64(tag & 0xFF) << np.uint64(48)) | g
+    return w.astype("<u8").view(np.uint8)
+
+
+def fill_normal_bf16_(t, seed: int, chunk_elems: int = 1 << 28) -> None:
+    """Fill a torch uint8 tensor (even size) with N(0,1) bf16 values drawn
+    from a torch generator on the tensor's device."""
+    import torch
+    v = t.view(torch.bfloat16)
+    g = torch.Generator(device=t.device)
+    g.manual_seed(seed)
+    for s in range(0, v.numel(), chunk_elems):
+        e = min(v.numel(), s + chunk_elems)
+        v[s:e].copy_(torch.randn(e - s, generator=g, device=t.device, dtype=torch.float32))
+
+
+def fill_random_bytes_(t, seed: int, chunk: int = 1 << 30) -> None:
+    import torch
+    g = torch.Generator(device=t.device)
+    g.manual_seed(seed)
+    for s in range(0, t.numel(), chunk):
+        e = min(t.numel(), s + chunk)
+        t[s:e].copy_(torch.randint(0, 256, (e - s,), generator=g, device=t.device,
+                                   dtype=torch.uint8))
+
+
+def fill_prefill_(t, tag: int, chunk_groups: int = 1 << 27) -> None:
+    """The offset-coded prefill of ``prefill_bytes`` written into a torch
+    uint8 tensor on its own device."""
+    import torch
+    if t.numel() % 8:
+        raise ValueError("prefill covers whole 8-byte groups")
+    w = t.view(torch.int64)
+    hi = (0x5A << 56) | ((tag & 0xFF) << 48)
+    for s in range(0, w.numel(), chunk_groups):
+        e = min(w.numel(), s + chunk_groups)
+        w[s:e].copy_(torch.arange(s, e, device=t.device, dtype=torch.int64) | hi)

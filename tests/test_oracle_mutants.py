@@ -1,0 +1,105 @@
+"""Plant plausible mistakes in the CPU oracle and check that its pins notice.
+
+Each mutant is one textual edit of ``oracle/kvx_oracle.c`` (a dropped term, a
+transposed operand, a wrong index, an off-by-one, a missing check).  The
+mutant is compiled into a temporary directory and the whole pin suite runs
+against it in a child process (a mutant may crash; that counts as caught).
+The real oracle must pass the same suite.
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+from oracle import kvx_oracle
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+PINS = os.path.join(HERE, "oracle_pins.py")
+
+T_LPCTHD = ("case ORA_LPCTHD:\n        return ((((l * P->N + p) * P->C + c) * P->T + s)"
+            " * P->H + h) * P->D + d;")
+T_LPCHTD = ("case ORA_LPCHTD:\n        return ((((l * P->N + p) * P->C + c) * P->H + h)"
+            " * P->T + s) * P->D + d;")
+T_PLCTHD = "case ORA_PLCTHD:\n        return ((((p * P->L + l) * P->C + c) * P->T + s) * P->H + h)"
+T_PLCHTD = "case ORA_PLCHTD:\n        return ((((p * P->L + l)"
+T_RESOLVE = ("            int bad = resolve(Dp, dst_pt, dst_pt_len, q[R_DST_PT], pd,\n"
+             "                              ORA_ERR_DST_PAGE, &dp, &ds);\n"
+             "            if (!bad)\n"
+             "                bad = resolve(S, src_pt, src_pt_len, q[R_SRC_PT], ps,\n"
+             "                              ORA_ERR_SRC_PAGE, &sp, &ss);")
+T_XFER_H = ("for (int64_t h = 0; h < S->H; ++h)\n"
+            "                        for (int64_t d = 0; d < S->D; ++d)\n"
+            "                            copy_elem(dst + Dp->e * pool_index(Dp")
+
+MUTANTS = {
+    "lpcthd_slot_head_swapped": (T_LPCTHD, T_LPCTHD.replace(
+        "* P->T + s) * P->H + h)", "* P->H + h) * P->T + s)")),
+    "lpcthd_kv_dropped": (T_LPCTHD, T_LPCTHD.replace("* P->C + c)", "* P->C)")),
+    "lpchtd_dim_dropped": (T_LPCHTD, T_LPCHTD.replace("* P->D + d;", "* P->D;")),
+    "plcthd_head_major": (T_PLCTHD, T_PLCTHD.replace(
+        "* P->T + s) * P->H + h)", "* P->H + h) * P->T + s)")),
+    "plchtd_layer_major": (T_PLCHTD, T_PLCHTD.replace("(p * P->L + l)", "(l * P->N + p)")),
+    "buffer_layer_kv_swapped": ("return off + (((l * B->C + c) * n + i)",
+                                "return off + (((c * B->L + l) * n + i)"),
+    "buffer_head_major": ("(((l * B->C + c) * n + i) * B->H + h) * B->D + d",
+                          "(((l * B->C + c) * B->H + h) * n + i) * B->D + d"),
+    "slot_off_by_one": ("*slot = q % P->T;", "*slot = (q + 1) % P->T;"),
+    "page_index_rounds_up": ("int64_t idx = pt_off + q / P->T;",
+                             "int64_t idx = pt_off + (q + P->T - 1) / P->T;"),
+    "source_position_from_dst_start": (
+        "int64_t ps = q[R_SRC_START] + i, pd = q[R_DST_START] + i;",
+        "int64_t ps = q[R_DST_START] + i, pd = q[R_DST_START] + i;"),
+    "dst_position_from_src_start": (
+        "int64_t ps = q[R_SRC_START] + i, pd = q[R_DST_START] + i;",
+        "int64_t ps = q[R_SRC_START] + i, pd = q[R_SRC_START] + i;"),
+    "element_last_byte_dropped": ("for (int64_t b = 0; b < e; ++b)",
+                                  "for (int64_t b = 0; b + 1 < e; ++b)"),
+    "transfer_one_head_short": (T_XFER_H, T_XFER_H.replace("h < S->H", "h + 1 < S->H")),
+    "scatter_tokens_reversed": (
+        "src + B->e * buf_index(B, q[R_BUF], n, l, c, i, h, d)",
+        "src + B->e * buf_index(B, q[R_BUF], n, l, c, n - 1 - i, h, d)"),
+    "block_may_not_reach_end": ("<= B->cap;", "< B->cap;"),
+    "gather_ignores_dst_start": ("q[R_DST_START] != 0 ||", "0 ||"),
+    "page_id_n_accepted": ("if (id < 0 || id >= P->N)", "if (id < 0 || id > P->N)"),
+    "table_end_accepted": ("if (idx < 0 || idx >= pt_len)", "if (idx < 0 || idx > pt_len)"),
+    "source_resolved_first": (T_RESOLVE, T_RESOLVE
+                              .replace("resolve(Dp, dst_pt, dst_pt_len, q[R_DST_PT], pd,\n"
+                                       "                              ORA_ERR_DST_PAGE, &dp, &ds)",
+                                       "@@D@@")
+                              .replace("resolve(S, src_pt, src_pt_len, q[R_SRC_PT], ps,\n"
+                                       "                              ORA_ERR_SRC_PAGE, &sp, &ss)",
+                                       "resolve(Dp, dst_pt, dst_pt_len, q[R_DST_PT], pd,\n"
+                                       "                              ORA_ERR_DST_PAGE, &dp, &ds)")
+                              .replace("@@D@@",
+                                       "resolve(S, src_pt, src_pt_len, q[R_SRC_PT], ps,\n"
+                                       "                              ORA_ERR_SRC_PAGE, &sp, &ss)")),
+    "negative_start_accepted": ("return n >= 0 && start >= 0 &&", "return n >= 0 &&"),
+    "int32_end_unchecked": ("&& start + n <= INT32_MAX;", ";"),
+    "misaligned_block_accepted": ("if (off < 0 || (off * B->e) % 16 != 0)", "if (off < 0)"),
+}
+
+
+def _run_pins(lib):
+    return subprocess.run([sys.executable, PINS, lib], capture_output=True, text=True,
+                          timeout=300)
+
+
+def test_real_oracle_passes_pins_in_child():
+    kvx_oracle.build()
+    r = _run_pins(kvx_oracle.LIBRARY)
+    assert r.returncode == 0, r.stdout + r.stderr
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, tmp_path):
+    old, new = MUTANTS[name]
+    text = open(kvx_oracle.SOURCE).read()
+    assert text.count(old) == 1, f"mutation site for {name} must occur exactly once"
+    assert old != new
+    src = tmp_path / "kvx_oracle_mutant.c"
+    src.write_text(text.replace(old, new))
+    lib = str(tmp_path / "libkvx_oracle_mutant.so")
+    kvx_oracle.build(str(src), lib)
+    r = _run_pins(lib)
+    assert r.returncode != 0, f"mutant {name} survived every pin"
