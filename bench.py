@@ -1,0 +1,288 @@
+#!/usr/bin/env python3
+"""Throughput of the paged KV-cache transfer path on one MI355X.
+
+One step is one pass of the whole path over one batch of requests on
+synthetic pools already resident in HBM.  The default workload is the LLM
+role handoff:
+- 36 layers x 8 KV heads x 128 head_dim, bf16;
+- 4096 x 64-token pools on both sides, layout [layer][page][kv][token][head][dim];
+- 32 requests with lengths uniform in [1024, 8192] on random page tables.
+A step is one fused kvx_transfer of all 32 requests.  ``--config 3/4/5``
+selects the relayout, MLA partial-prefix and host-tier workloads.
+
+GB/s counts algorithmic bytes, GB = 1e9: every copied token position is read
+once and written once, 2 * tokens * L*C*H*D*e per step.
+
+Printed as one JSON line:
+- ``roofline``: the transfer kernel's own rate.  Its bytes per launch are
+  divided by the average launch duration, measured with HIP events on the
+  launch stream, and compared with the 8 TB/s HBM peak.
+- ``cpu_baseline``: the CPU oracle timed on this host over a sample of
+  layers.  The same layers are also compared bit for bit with the GPU
+  result.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "KV transfer GB/s (read+write) and % of HBM/host-link peak, 1 MI355X"
+HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, published
+PCIE_PEAK_GBPS = 63.0         # PCIe 5.0 x16 per direction: 32 GT/s x 16 x 128/130 / 8
+KERNEL_SOURCES = ["paper_2606_31093_amd/csrc/kvx_kernels.hip",
+                  "paper_2606_31093_amd/csrc/kvx_internal.h",
+                  "paper_2606_31093_amd/csrc/kvx_api.cpp", "include/kvx.h"]
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def kernel_sha() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_record(key: int):
+    """HBM bytes per launch from the committed rocprofv3 counter summary,
+    if it was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"traffic_config{key}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("kernel_sha") != kernel_sha():
+        return None
+    return rec
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4, 5])
+    ap.add_argument("--cpu-layers", type=int, default=16,
+                    help="layers of the workload the CPU oracle runs (0: skip)")
+    ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
+    ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
+                    help="only run a plain device copy of this many GiB (counter calibration)")
+    return ap.parse_args()
+
+
+def calibrate_copy(gib: float) -> None:
+    """A plain copy kernel of known size, for scaling rocprofv3 byte counters."""
+    import torch
+    n = int(gib * 2**30)
+    a = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes": n, "launches": 3}), flush=True)
+
+
+def main() -> int:
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
+                          "n_gpus": args.gpus}), flush=True)
+        return 2
+    if int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only (WORLD_SIZE must be 1)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    if args.calibrate_copy > 0:
+        calibrate_copy(args.calibrate_copy)
+        return 0
+
+    from paper_2606_31093_amd import build_lib, kvx, workloads
+
+    if not os.path.exists(build_lib.LIBRARY):
+        log("libkvx.so missing: building")
+        build_lib.build()
+    kvx.lib()
+
+    dev = torch.device("cuda", 0)
+    wl = workloads.config(args.config)
+    log(f"workload: {wl.title}")
+    mem = {}
+    for name, spec in wl.sides.items():
+        pinned = name in wl.host_sides
+        log(f"allocating side {name}: {spec.nbytes / 2**30:.2f} GiB "
+            f"{'pinned host' if pinned else 'HBM'}")
+        mem[name] = workloads.alloc_side(spec, dev, pinned=pinned)
+    log("filling source values and destination prefill")
+    workloads.init_sides_(wl, mem)
+    dsteps = []
+    for st in wl.steps:
+        dsteps.append(dict(
+            st=st,
+            spt=kvx.device_table(st.src_pt, dev) if st.src_pt is not None else None,
+            dpt=kvx.device_table(st.dst_pt, dev) if st.dst_pt is not None else None,
+            reqs=kvx.device_reqs(st.reqs, dev)))
+    errw = torch.zeros(1, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+
+    def launch(d):
+        st = d["st"]
+        S, D = wl.sides[st.src], wl.sides[st.dst]
+        if st.op == "transfer":
+            kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"], errw)
+        elif st.op == "gather":
+            kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, d["spt"], d["reqs"], errw)
+        else:
+            kvx.kvx_scatter(mem[st.src], S, mem[st.dst], D, d["dpt"], d["reqs"], errw)
+
+    log(f"warmup: {args.warmup} steps")
+    for _ in range(args.warmup):
+        for d in dsteps:
+            launch(d)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    events = [[] for _ in dsteps]
+    log(f"timing: {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        for i, d in enumerate(dsteps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            launch(d)
+            e1.record(stream)
+            events[i].append((e0, e1))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    dev_err = int(errw.item())
+    if dev_err:
+        log(f"device error bits {dev_err}")
+        return 1
+
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    step_bytes = sum(wl.algorithmic_bytes(st) for st in wl.steps)
+    value = step_bytes / (ms_per_step / 1e3) / 1e9
+    kern_ms = [sum(a.elapsed_time(b) for a, b in ev) / len(ev) for ev in events]
+    log(f"{ms_per_step:.3f} ms/step, {value:.1f} GB/s; kernel ms {kern_ms}")
+
+    # dominant kernel
+    i_dom = max(range(len(dsteps)), key=lambda i: kern_ms[i])
+    dom = wl.steps[i_dom]
+    dom_bytes = wl.algorithmic_bytes(dom)
+    achieved = dom_bytes / (kern_ms[i_dom] / 1e3) / 1e9
+    host_leg = bool(wl.host_sides)
+    tr = traffic_record(args.config)
+    if host_leg:
+        one_way = dom_bytes / 2
+        roofline = {"bound": "pcie", "achieved": round(one_way / (kern_ms[i_dom] / 1e3) / 1e9, 2),
+                    "peak": PCIE_PEAK_GBPS, "unit": "GB/s",
+                    "frac": round(one_way / (kern_ms[i_dom] / 1e3) / 1e9 / PCIE_PEAK_GBPS, 4),
+                    "traffic": tr["traffic_bytes_per_launch"] if tr else None,
+                    "kernel": f"kvx {dom.op}", "bytes_per_launch": int(one_way),
+                    "kernel_ms": round(kern_ms[i_dom], 4)}
+    else:
+        roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                    "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                    "traffic": tr["traffic_bytes_per_launch"] if tr else None,
+                    "kernel": f"kvx {dom.op}", "bytes_per_launch": int(dom_bytes),
+                    "kernel_ms": round(kern_ms[i_dom], 4)}
+
+    context = {"kernel_sha": kernel_sha(), "per_step_kernel_ms": [round(x, 4) for x in kern_ms]}
+    if not args.no_memcpy and not host_leg:
+        # hipMemcpyAsync D2D of the same byte count, as the achievable copy rate
+        st = wl.steps[0]
+        nb = min(dom_bytes // 2, mem[st.src].numel(), mem[st.dst].numel())
+        ev = []
+        cpy_a, cpy_b = mem[st.src][:nb], mem[st.dst][:nb]
+        reps = 5
+        for r in range(reps + 1):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            cpy_b.copy_(cpy_a)
+            e1.record(stream)
+            if r:
+                ev.append((e0, e1))
+        torch.cuda.synchronize()
+        ms = sum(a.elapsed_time(b) for a, b in ev) / reps
+        context["hip_memcpy_d2d_GBps_read_plus_write"] = round(2 * nb / (ms / 1e3) / 1e9, 1)
+        # the copy above overwrote the destination: redo one step for the checks below
+        workloads.fill_prefill_(mem[st.dst], wl.prefill_tag)
+        for d in dsteps:
+            launch(d)
+        torch.cuda.synchronize()
+
+    cpu = None
+    if args.cpu_layers > 0 and not host_leg:
+        from oracle import layer_check
+        st = wl.steps[0]
+        S, D = wl.sides[st.src], wl.sides[st.dst]
+        L = S.L
+        picks = sorted({round(i * (L - 1) / max(1, args.cpu_layers - 1))
+                        for i in range(min(args.cpu_layers, L))})
+        secs, moved, exact = 0.0, 0, True
+        for l in picks:
+            r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l,
+                                                 wl.prefill_tag)
+            log(f"cpu oracle layer {l}: {r.oracle_seconds:.2f} s, bit-exact={r.equal}")
+            secs += r.oracle_seconds
+            moved += r.moved_bytes
+            exact = exact and r.equal
+        if not exact:
+            log("GPU result differs from the oracle on a sampled layer")
+            return 1
+        cpu = {"value": round(moved / secs / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"layers {picks} of {L}: all {len(st.reqs)} requests, "
+                         f"{moved / 1e9:.2f} GB moved, {secs:.1f} s single-threaded",
+               "sample_bit_exact": exact,
+               "cpu_model": _cpu_model(), "host_cpu_count": os.cpu_count()}
+
+    n_tok = sum(st.n_tokens for st in wl.steps)
+    out = {
+        "metric": METRIC, "value": round(value, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u16",
+        "data": "synthetic (seeded N(0,1) bf16 source, offset-coded destination prefill)",
+        "config": {"workload": wl.title, "config": args.config,
+                   "ops": [st.op for st in wl.steps], "requests": len(wl.steps[0].reqs),
+                   "tokens_per_step": n_tok, "bytes_per_step": step_bytes,
+                   "pools": {k: {"bytes": v.nbytes, **({"layout": v.layout, "page_tokens": v.T}
+                                                       if hasattr(v, "layout") else {})}
+                             for k, v in wl.sides.items()},
+                   "host_sides": list(wl.host_sides)},
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "context": context,
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+def _cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,182 @@
+/*
+ * kvx.h -- paged KV-cache gather / scatter / transfer for MI355X (gfx950).
+ *
+ * These calls are the data movement under Omni-Flow's Data Flow layer.
+ * - Sec. 4.1.1 (Physical Paging Layer): a KV cache is addressed as the
+ *   Cartesian product layer x page x slice, and the paging layer owns the
+ *   cross-tier copy primitives.
+ * - Sec. 4.1.2 (Multi-Tier Slot Engine): migration converts between the
+ *   paged GPU layout and a flat per-request serialization.
+ * - Sec. 5.2 (Holistic KV-Cache Takeover): the data plane translates slots
+ *   to page ids.
+ * - Sec. 4.1.4 (Copy-on-Write and Fragmented Page Handling): a partial
+ *   write leaves the rest of its page as it was.
+ *
+ * Definition.  Take a request record r and a token offset i with
+ * 0 <= i < n_tokens.  The element at (layer l, kv c, position
+ * src_start + i, head h, dim d) of the source is copied to
+ * (l, c, dst_start + i, h, d) of the destination.
+ * - A pool side resolves position q through its page table:
+ *       page = table[pt_off + q / page_tokens],  slot = q % page_tokens
+ * - A buffer side holds the request's block [layer][kv][token][head][dim],
+ *   which starts at element buf_off and is indexed by i.
+ * - No other destination byte is written, and the source is only read.
+ * - Elements are opaque words of elem_bytes bytes, copied bit for bit.
+ *
+ * Ownership.
+ * - The caller owns every buffer, table, record array, error word and
+ *   stream.
+ * - The library allocates no device or host memory and keeps no state
+ *   between calls.  It keeps a thread-local error message and a per-device
+ *   launch-shape cache.
+ * - Page tables, request records and the error word must be readable and
+ *   writable by the device: device memory, or pinned host memory mapped for
+ *   the device.
+ * - Descriptors are read on the host during the call.
+ *
+ * Synchrony.
+ * - The entry points enqueue kernels on `stream` (a hipStream_t; NULL is
+ *   the default stream) and return without waiting.
+ * - Destination data and *dev_err are valid once the stream has
+ *   synchronised.
+ *
+ * Errors.
+ * - A call returns KVX_OK or a negative kvx_status, with nothing enqueued.
+ *   kvx_last_error() then names the failing check.
+ * - Problems that only the device can see skip the affected elements and
+ *   OR bits into *dev_err (when non-NULL):
+ *   - KVX_DERR_SRC_PAGE / KVX_DERR_DST_PAGE: a page id outside
+ *     [0, num_pages);
+ *   - KVX_DERR_PT_RANGE: a table index outside [0, pt_len);
+ *   - KVX_DERR_BAD_REQ: a malformed request record.  The whole record is
+ *     skipped.
+ * - The destination side is resolved before the source side, so a
+ *   position bad on both sides reports only the destination bit.
+ * - Not detected: two records that write the same destination slot, and
+ *   source and destination memory that overlap.  Both give undefined
+ *   results.
+ */
+#ifndef KVX_H
+#define KVX_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define KVX_ABI_VERSION 1
+
+/* Most request records per call (each workgroup walks the record array). */
+#define KVX_MAX_REQS 65536
+/* Largest page (tokens) a pool may declare. */
+#define KVX_MAX_PAGE_TOKENS (1 << 20)
+
+/* Memory order of a pool.  The letters name axes outermost first:
+ * L layer, P page, C kv component, T token slot, H head, D head_dim.
+ * D is innermost in every layout, so a (l, p, c, t, h) "row" of
+ * head_dim * elem_bytes bytes is always contiguous. */
+typedef enum kvx_layout {
+    KVX_LPCTHD = 0, /* [layer][page][kv][token][head][dim]: the NHD block stack */
+    KVX_LPCHTD = 1, /* [layer][page][kv][head][token][dim] */
+    KVX_PLCTHD = 2, /* [page][layer][kv][token][head][dim] */
+    KVX_PLCHTD = 3  /* [page][layer][kv][head][token][dim] */
+} kvx_layout;
+
+typedef enum kvx_status {
+    KVX_OK = 0,
+    KVX_ERR_NULL = -1,      /* a required pointer is NULL */
+    KVX_ERR_SHAPE = -2,     /* sides differ in layers/kv/heads/head_dim/elem_bytes,
+                               or a dimension is out of range */
+    KVX_ERR_ALIGN = -3,     /* a base pointer, or head_dim * elem_bytes, is not a
+                               multiple of 16 bytes */
+    KVX_ERR_LAYOUT = -4,    /* unknown layout, or num_kv not 1 or 2 */
+    KVX_ERR_RANGE = -5,     /* n_reqs, pt_len or a size out of range */
+    KVX_ERR_HIP = -6        /* the HIP runtime refused a query or a launch */
+} kvx_status;
+
+/* Device-side error bits. */
+#define KVX_DERR_SRC_PAGE 1u
+#define KVX_DERR_DST_PAGE 2u
+#define KVX_DERR_PT_RANGE 4u
+#define KVX_DERR_BAD_REQ 8u
+
+/* A paged pool of num_pages pages; element (l, p, c, t, h, d) lives where
+ * `layout` puts it.  `base` is device memory, 16-byte aligned. */
+typedef struct kvx_pool {
+    void *base;
+    int32_t num_layers;  /* L >= 1 */
+    int32_t num_kv;      /* C: 2 (K and V) or 1 (one latent, as in MLA) */
+    int32_t num_heads;   /* H >= 1 */
+    int32_t head_dim;    /* D >= 1; D * elem_bytes a multiple of 16 */
+    int32_t page_tokens; /* T, 1 .. KVX_MAX_PAGE_TOKENS */
+    int32_t num_pages;   /* N >= 1 */
+    int32_t elem_bytes;  /* 1, 2, 4 or 8 */
+    int32_t layout;      /* a kvx_layout */
+} kvx_pool;
+
+/* A flat buffer of per-request blocks [layer][kv][token][head][dim] (the
+ * flat serialization used by host tiers).  `base` is device memory or
+ * device-mapped pinned host memory, 16-byte aligned. */
+typedef struct kvx_buf {
+    void *base;
+    int32_t num_layers, num_kv, num_heads, head_dim, elem_bytes;
+    int32_t reserved;        /* 0 */
+    int64_t capacity_elems;  /* elements addressable from base */
+} kvx_buf;
+
+/* One request record (40 bytes).  A record is malformed (KVX_DERR_BAD_REQ)
+ * if n_tokens < 0, a start is negative, a start + n_tokens exceeds
+ * 2^31 - 1, `reserved` is not 0, or, for a buffer side, its start is not 0
+ * or its block [buf_off, buf_off + L*C*n_tokens*H*D) is not 16-byte aligned
+ * or does not fit the buffer. */
+typedef struct kvx_req {
+    int64_t src_pt_off; /* index in src_pt of the request's logical page 0 */
+    int64_t dst_pt_off; /* index in dst_pt of the request's logical page 0 */
+    int64_t buf_off;    /* element offset of the request's block (buffer side) */
+    int32_t src_start;  /* first position read (0 for a buffer source) */
+    int32_t dst_start;  /* first position written (0 for a buffer destination) */
+    int32_t n_tokens;   /* positions moved; 0 moves nothing */
+    int32_t reserved;   /* must be 0 */
+} kvx_req;
+
+/* Pool -> pool, with any change of page size and layout.
+ * Sec. 4.1 (role-to-role sharing through the Global Params Pool); Sec. 5.1
+ * (partial-prefix reuse: src_start/dst_start select [p, len)).
+ * src_pt / dst_pt: int32 page tables of src_pt_len / dst_pt_len entries.
+ * reqs: n_reqs records (0 <= n_reqs <= KVX_MAX_REQS). */
+int kvx_transfer(const kvx_pool *src, const kvx_pool *dst,
+                 const int32_t *src_pt, int64_t src_pt_len,
+                 const int32_t *dst_pt, int64_t dst_pt_len,
+                 const kvx_req *reqs, int32_t n_reqs,
+                 uint32_t *dev_err, void *stream);
+
+/* Pool -> flat buffer: the offload (serialization) direction of Sec. 4.1.2. */
+int kvx_gather(const kvx_pool *src, const kvx_buf *dst,
+               const int32_t *src_pt, int64_t src_pt_len,
+               const kvx_req *reqs, int32_t n_reqs,
+               uint32_t *dev_err, void *stream);
+
+/* Flat buffer -> pool: the onload direction of Sec. 4.1.2. */
+int kvx_scatter(const kvx_buf *src, const kvx_pool *dst,
+                const int32_t *dst_pt, int64_t dst_pt_len,
+                const kvx_req *reqs, int32_t n_reqs,
+                uint32_t *dev_err, void *stream);
+
+/* Bytes a pool described by *pool occupies (-1 if the descriptor is invalid). */
+int64_t kvx_pool_bytes(const kvx_pool *pool);
+
+/* Static text for a kvx_status value. */
+const char *kvx_strerror(int status);
+
+/* The calling thread's message for its last failed call ("" if none). */
+const char *kvx_last_error(void);
+
+/* KVX_ABI_VERSION of the loaded library. */
+int kvx_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVX_H */

@@ -1,0 +1,87 @@
+"""Per-layer checking of full-size runs against the CPU oracle.
+
+TEST INFRASTRUCTURE ONLY (tests, smoke, the benchmark's CPU-baseline leg).
+Layers never mix in the copy: layer l of the destination depends only on
+layer l of the source.  A layer slice of any pool is itself a pool of the
+same layout with one layer, and the layer-l part of each request's flat
+block is itself a one-layer block.  So a run over pools of tens of GiB is
+checked one layer at a time: copy the layer slices to the host, run the
+oracle with one-layer shapes from the regenerated destination prefill, and
+compare bytes.
+"""
+from __future__ import annotations
+
+import dataclasses
+import time
+
+import numpy as np
+
+from oracle import kvx_oracle
+from paper_2606_31093_amd.workloads import BufSpec, prefill_words
+
+
+def one_layer(spec):
+    return dataclasses.replace(spec, L=1) if not isinstance(spec, BufSpec) else \
+        dataclasses.replace(spec, L=1, cap=spec.cap // spec.L)
+
+
+def layer_major(spec) -> bool:
+    return spec.layout.startswith("L")
+
+
+def pool_layer(t, spec, l: int) -> np.ndarray:
+    """Host bytes of layer l of a pool held in torch uint8 tensor t."""
+    per = spec.nbytes // spec.L
+    if layer_major(spec):
+        return t[l * per:(l + 1) * per].cpu().numpy()
+    per_page = per // spec.N
+    return t.view(spec.N, spec.L, per_page)[:, l, :].contiguous().cpu().numpy().reshape(-1)
+
+
+def pool_layer_prefill(spec, l: int, tag: int) -> np.ndarray:
+    """The offset-coded prefill of layer l of a pool (as ``fill_prefill_``
+    wrote it over the whole pool)."""
+    per = spec.nbytes // spec.L
+    if layer_major(spec):
+        g = np.arange(l * per // 8, (l + 1) * per // 8, dtype=np.uint64)
+    else:
+        per_page = per // spec.N
+        g = ((np.arange(spec.N, dtype=np.uint64)[:, None] * spec.L + l) * (per_page // 8)
+             + np.arange(per_page // 8, dtype=np.uint64)[None, :]).reshape(-1)
+    return prefill_words(g, tag).view(np.uint8).copy()
+
+
+def buf_layer(t, spec, l: int, blocks) -> tuple[np.ndarray, list]:
+    """Layer l of every request block of a flat buffer, packed back to back.
+    ``blocks`` lists (element offset, n_tokens) per request; returns the
+    packed bytes and the one-layer block offsets (elements)."""
+    per_tok = spec.C * spec.H * spec.D * spec.e
+    parts, offs, pos = [], [], 0
+    for off, n in blocks:
+        start = off * spec.e + l * n * per_tok
+        parts.append(t[start:start + n * per_tok].cpu().numpy())
+        offs.append(pos // spec.e)
+        pos += n * per_tok
+    return (np.concatenate(parts) if parts else np.zeros(0, np.uint8)), offs
+
+
+@dataclasses.dataclass
+class LayerResult:
+    layer: int
+    equal: bool
+    oracle_seconds: float
+    moved_bytes: int      # algorithmic bytes (read + write) of this layer
+
+
+def check_transfer_layer(src_t, S, dst_t, D, step, l: int, tag: int) -> LayerResult:
+    """Run the oracle on layer l of a pool -> pool step and compare it with
+    the device result."""
+    s1, d1 = one_layer(S), one_layer(D)
+    src = pool_layer(src_t, S, l)
+    got = pool_layer(dst_t, D, l)
+    want = pool_layer_prefill(D, l, tag)
+    t0 = time.perf_counter()
+    err = kvx_oracle.default().transfer(src, s1, want, d1, step.src_pt, step.dst_pt, step.reqs)
+    dt = time.perf_counter() - t0
+    moved = 2 * int(step.reqs[:, 5].sum()) * S.C * S.H * S.D * S.e
+    return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved)

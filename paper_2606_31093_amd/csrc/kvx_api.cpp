@@ -1,0 +1,355 @@
+// kvx_api.cpp -- the C-ABI of libkvx (include/kvx.h): host-side validation
+// of descriptors, derivation of byte strides per layout, and the launch of
+// the copy kernel on the caller's stream.  Nothing is allocated here.
+
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <string>
+
+#include "kvx.h"
+#include "kvx_internal.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int status, const char *fmt, ...) {
+    char msg[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(msg, sizeof msg, fmt, ap);
+    va_end(ap);
+    g_last_error = msg;
+    return status;
+}
+
+// a * b for non-negative operands, or -1 if the product exceeds int64.
+int64_t mul_checked(int64_t a, int64_t b) {
+    if (a < 0 || b < 0) return -1;
+    if (a != 0 && b > INT64_MAX / a) return -1;
+    return a * b;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Element shape shared by both sides of a call.
+struct Shape {
+    int32_t L, C, H, D, e;
+};
+
+int check_shape(const char *name, const Shape &s) {
+    if (s.L < 1 || s.H < 1 || s.D < 1)
+        return fail(KVX_ERR_SHAPE, "%s: num_layers, num_heads and head_dim must be >= 1", name);
+    if (s.C != 1 && s.C != 2) return fail(KVX_ERR_LAYOUT, "%s: num_kv must be 1 or 2 (got %d)", name, s.C);
+    if (s.e != 1 && s.e != 2 && s.e != 4 && s.e != 8)
+        return fail(KVX_ERR_SHAPE, "%s: elem_bytes must be 1, 2, 4 or 8 (got %d)", name, s.e);
+    const int64_t row = (int64_t)s.D * s.e;
+    if (row % 16 != 0)
+        return fail(KVX_ERR_ALIGN, "%s: head_dim * elem_bytes = %lld is not a multiple of 16", name,
+                    (long long)row);
+    const int64_t token = mul_checked(mul_checked(mul_checked(s.L, s.C), s.H), row);
+    if (token < 0 || token > (int64_t(1) << 31))
+        return fail(KVX_ERR_SHAPE, "%s: one token spans more than 2 GiB across all layers", name);
+    return KVX_OK;
+}
+
+int pool_shape(const kvx_pool *p, const char *name, Shape &s) {
+    if (!p) return fail(KVX_ERR_NULL, "%s: pool descriptor is NULL", name);
+    s = Shape{p->num_layers, p->num_kv, p->num_heads, p->head_dim, p->elem_bytes};
+    int st = check_shape(name, s);
+    if (st) return st;
+    if (p->layout < KVX_LPCTHD || p->layout > KVX_PLCHTD)
+        return fail(KVX_ERR_LAYOUT, "%s: unknown layout %d", name, p->layout);
+    if (p->page_tokens < 1 || p->page_tokens > KVX_MAX_PAGE_TOKENS)
+        return fail(KVX_ERR_SHAPE, "%s: page_tokens %d outside [1, %d]", name, p->page_tokens,
+                    KVX_MAX_PAGE_TOKENS);
+    if (p->num_pages < 1) return fail(KVX_ERR_SHAPE, "%s: num_pages must be >= 1", name);
+    // A tile (one page of one layer) must stay below 2^31 16-byte vectors.
+    const int64_t tile_vecs = (int64_t)s.C * p->page_tokens * s.H * (s.D * s.e / 16);
+    if (tile_vecs >= (int64_t(1) << 31))
+        return fail(KVX_ERR_SHAPE, "%s: one page of one layer exceeds 32 GiB", name);
+    return KVX_OK;
+}
+
+int64_t pool_bytes(const kvx_pool *p) {
+    int64_t b = mul_checked(mul_checked(mul_checked(p->num_layers, p->num_kv), p->num_heads),
+                            (int64_t)p->head_dim * p->elem_bytes);
+    b = mul_checked(mul_checked(b, p->page_tokens), p->num_pages);
+    return b;
+}
+
+int same_shape(const Shape &a, const Shape &b) {
+    if (a.L != b.L || a.C != b.C || a.H != b.H || a.D != b.D || a.e != b.e)
+        return fail(KVX_ERR_SHAPE,
+                    "source and destination differ in element shape: (L,C,H,D,e) = "
+                    "(%d,%d,%d,%d,%d) vs (%d,%d,%d,%d,%d)",
+                    a.L, a.C, a.H, a.D, a.e, b.L, b.C, b.H, b.D, b.e);
+    return KVX_OK;
+}
+
+// The device must be able to address `ptr` (device memory or mapped pinned
+// host memory).  On success *dev_ptr is the address kernels use.
+int device_view(const void *ptr, const char *name, void **dev_ptr) {
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, ptr);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();  // clear the sticky error the query leaves
+        return fail(KVX_ERR_RANGE, "%s (%p) is not memory the GPU can address (%s)", name, ptr,
+                    hipGetErrorString(e));
+    }
+    if (attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged ||
+        attr.type == hipMemoryTypeUnified) {
+        *dev_ptr = const_cast<void *>(ptr);
+        return KVX_OK;
+    }
+    if (attr.type == hipMemoryTypeHost && attr.devicePointer) {
+        *dev_ptr = attr.devicePointer;
+        return KVX_OK;
+    }
+    return fail(KVX_ERR_RANGE, "%s (%p) is not device memory or mapped pinned host memory", name, ptr);
+}
+
+// Byte strides of (layer, page, kv, slot, head) for a pool layout.
+kvx::Side pool_side(const kvx_pool *p, void *base, const int32_t *pt, int64_t pt_len) {
+    const int64_t row = (int64_t)p->head_dim * p->elem_bytes;
+    const int64_t L = p->num_layers, N = p->num_pages, C = p->num_kv, T = p->page_tokens,
+                  H = p->num_heads;
+    kvx::Side s{};
+    s.base = static_cast<char *>(base);
+    const bool token_major = p->layout == KVX_LPCTHD || p->layout == KVX_PLCTHD;
+    if (token_major) {
+        s.s_h = row;
+        s.s_t = H * row;
+    } else {
+        s.s_t = row;
+        s.s_h = T * row;
+    }
+    s.s_c = T * H * row;
+    if (p->layout == KVX_LPCTHD || p->layout == KVX_LPCHTD) {
+        s.s_p = C * s.s_c;
+        s.s_l = N * s.s_p;
+    } else {
+        s.s_l = C * s.s_c;
+        s.s_p = L * s.s_l;
+    }
+    s.pt = pt;
+    s.pt_len = pt_len;
+    s.T = p->page_tokens;
+    s.N = p->num_pages;
+    s.is_buf = 0;
+    s.tok_contig = token_major || H == 1;
+    s.cap_bytes = 0;
+    return s;
+}
+
+kvx::Side buf_side(const kvx_buf *b, void *base) {
+    kvx::Side s{};
+    s.base = static_cast<char *>(base);
+    s.is_buf = 1;
+    s.tok_contig = 1;
+    s.T = 1;
+    s.N = 0;
+    s.cap_bytes = b->capacity_elems * b->elem_bytes;
+    return s;
+}
+
+// Host-only checks of a pool descriptor (no HIP call).
+int check_pool(const kvx_pool *p, const char *name, Shape &s) {
+    int st = pool_shape(p, name, s);
+    if (st) return st;
+    if (!p->base) return fail(KVX_ERR_NULL, "%s: base is NULL", name);
+    if (!aligned16(p->base)) return fail(KVX_ERR_ALIGN, "%s: base %p is not 16-byte aligned", name, p->base);
+    if (pool_bytes(p) < 0) return fail(KVX_ERR_RANGE, "%s: pool size exceeds 2^63 bytes", name);
+    return KVX_OK;
+}
+
+// Host-only checks of a buffer descriptor.
+int check_buf(const kvx_buf *b, const char *name, Shape &s) {
+    if (!b) return fail(KVX_ERR_NULL, "%s: buffer descriptor is NULL", name);
+    s = Shape{b->num_layers, b->num_kv, b->num_heads, b->head_dim, b->elem_bytes};
+    int st = check_shape(name, s);
+    if (st) return st;
+    if (b->reserved != 0) return fail(KVX_ERR_RANGE, "%s: reserved field must be 0", name);
+    if (!b->base) return fail(KVX_ERR_NULL, "%s: base is NULL", name);
+    if (!aligned16(b->base)) return fail(KVX_ERR_ALIGN, "%s: base %p is not 16-byte aligned", name, b->base);
+    if (b->capacity_elems < 0 || mul_checked(b->capacity_elems, b->elem_bytes) < 0)
+        return fail(KVX_ERR_RANGE, "%s: capacity_elems out of range", name);
+    return KVX_OK;
+}
+
+// Host-only checks of a page table.
+int check_table(const int32_t *pt, int64_t len, const char *name) {
+    if (len < 0) return fail(KVX_ERR_RANGE, "%s: negative length", name);
+    if (len > 0 && !pt) return fail(KVX_ERR_NULL, "%s is NULL but has %lld entries", name, (long long)len);
+    if ((reinterpret_cast<uintptr_t>(pt) & 3u) != 0) return fail(KVX_ERR_ALIGN, "%s is not 4-byte aligned", name);
+    return KVX_OK;
+}
+
+// Host-only checks of the record array and the error word.
+int check_common(const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err) {
+    if (n_reqs < 0 || n_reqs > KVX_MAX_REQS)
+        return fail(KVX_ERR_RANGE, "n_reqs %d outside [0, %d]", n_reqs, KVX_MAX_REQS);
+    if (n_reqs > 0 && !reqs) return fail(KVX_ERR_NULL, "reqs is NULL");
+    if ((reinterpret_cast<uintptr_t>(reqs) & 7u) != 0) return fail(KVX_ERR_ALIGN, "reqs is not 8-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(dev_err) & 3u) != 0)
+        return fail(KVX_ERR_ALIGN, "dev_err is not 4-byte aligned");
+    return KVX_OK;
+}
+
+// Device views of every pointer a launch uses.
+struct Views {
+    void *src = nullptr, *dst = nullptr;
+    const int32_t *src_pt = nullptr, *dst_pt = nullptr;
+    const kvx_req *reqs = nullptr;
+    uint32_t *err = nullptr;
+};
+
+int view_all(const void *src, const void *dst, const int32_t *src_pt, int64_t src_pt_len,
+             const int32_t *dst_pt, int64_t dst_pt_len, const kvx_req *reqs, uint32_t *dev_err,
+             Views &v) {
+    int st;
+    void *d = nullptr;
+    if ((st = device_view(src, "src base", &v.src))) return st;
+    if ((st = device_view(dst, "dst base", &v.dst))) return st;
+    if (src_pt_len > 0) {
+        if ((st = device_view(src_pt, "src_pt", &d))) return st;
+        v.src_pt = static_cast<const int32_t *>(d);
+    }
+    if (dst_pt_len > 0) {
+        if ((st = device_view(dst_pt, "dst_pt", &d))) return st;
+        v.dst_pt = static_cast<const int32_t *>(d);
+    }
+    if ((st = device_view(reqs, "reqs", &d))) return st;
+    v.reqs = static_cast<const kvx_req *>(d);
+    if (dev_err) {
+        if ((st = device_view(dev_err, "dev_err", &d))) return st;
+        v.err = static_cast<uint32_t *>(d);
+    }
+    return KVX_OK;
+}
+
+void finish_params(kvx::Params &P, const Shape &s, const Views &v, int32_t n_reqs) {
+    P.reqs = v.reqs;
+    P.err = v.err;
+    P.n_reqs = n_reqs;
+    P.L = s.L;
+    P.C = s.C;
+    P.H = s.H;
+    P.row_bytes = s.D * s.e;
+    P.vpr = P.row_bytes / 16;
+    P.elem_bytes = s.e;
+    P.flat = P.src.tok_contig && P.dst.tok_contig;
+    const kvx::Side &ts = P.op == kvx::OP_GATHER ? P.src : P.dst;
+    const kvx::Side &os = P.op == kvx::OP_GATHER ? P.dst : P.src;
+    P.fd_vpr = kvx::make_fastdiv((uint32_t)P.vpr);
+    P.fd_H = kvx::make_fastdiv((uint32_t)P.H);
+    P.fd_Tt = kvx::make_fastdiv((uint32_t)ts.T);
+    P.fd_To = kvx::make_fastdiv((uint32_t)os.T);
+    P.fd_HV = kvx::make_fastdiv((uint32_t)(P.H * P.vpr));
+}
+
+int enqueue(const kvx::Params &P, void *stream) {
+    int e = kvx::launch(P, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail(KVX_ERR_HIP, "kernel launch failed: %s", hipGetErrorString((hipError_t)e));
+    return KVX_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvx_transfer(const kvx_pool *src, const kvx_pool *dst, const int32_t *src_pt, int64_t src_pt_len,
+                 const int32_t *dst_pt, int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs,
+                 uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    Shape ss, ds;
+    int st;
+    if ((st = check_pool(src, "src", ss))) return st;
+    if ((st = check_pool(dst, "dst", ds))) return st;
+    if ((st = same_shape(ss, ds))) return st;
+    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
+    if ((st = check_table(src_pt, src_pt_len, "src_pt"))) return st;
+    if ((st = check_table(dst_pt, dst_pt_len, "dst_pt"))) return st;
+    if (n_reqs == 0) return KVX_OK;
+    Views v;
+    if ((st = view_all(src->base, dst->base, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, dev_err, v)))
+        return st;
+    kvx::Params P{};
+    P.op = kvx::OP_TRANSFER;
+    P.src = pool_side(src, v.src, v.src_pt, src_pt_len);
+    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len);
+    finish_params(P, ss, v, n_reqs);
+    return enqueue(P, stream);
+}
+
+int kvx_gather(const kvx_pool *src, const kvx_buf *dst, const int32_t *src_pt, int64_t src_pt_len,
+               const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    Shape ss, ds;
+    int st;
+    if ((st = check_pool(src, "src", ss))) return st;
+    if ((st = check_buf(dst, "dst", ds))) return st;
+    if ((st = same_shape(ss, ds))) return st;
+    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
+    if ((st = check_table(src_pt, src_pt_len, "src_pt"))) return st;
+    if (n_reqs == 0) return KVX_OK;
+    Views v;
+    if ((st = view_all(src->base, dst->base, src_pt, src_pt_len, nullptr, 0, reqs, dev_err, v)))
+        return st;
+    kvx::Params P{};
+    P.op = kvx::OP_GATHER;
+    P.src = pool_side(src, v.src, v.src_pt, src_pt_len);
+    P.dst = buf_side(dst, v.dst);
+    finish_params(P, ss, v, n_reqs);
+    return enqueue(P, stream);
+}
+
+int kvx_scatter(const kvx_buf *src, const kvx_pool *dst, const int32_t *dst_pt, int64_t dst_pt_len,
+                const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    Shape ss, ds;
+    int st;
+    if ((st = check_buf(src, "src", ss))) return st;
+    if ((st = check_pool(dst, "dst", ds))) return st;
+    if ((st = same_shape(ss, ds))) return st;
+    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
+    if ((st = check_table(dst_pt, dst_pt_len, "dst_pt"))) return st;
+    if (n_reqs == 0) return KVX_OK;
+    Views v;
+    if ((st = view_all(src->base, dst->base, nullptr, 0, dst_pt, dst_pt_len, reqs, dev_err, v)))
+        return st;
+    kvx::Params P{};
+    P.op = kvx::OP_SCATTER;
+    P.src = buf_side(src, v.src);
+    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len);
+    finish_params(P, ss, v, n_reqs);
+    return enqueue(P, stream);
+}
+
+int64_t kvx_pool_bytes(const kvx_pool *pool) {
+    Shape s;
+    if (!pool || pool_shape(pool, "pool", s) != KVX_OK) return -1;
+    return pool_bytes(pool);
+}
+
+const char *kvx_strerror(int status) {
+    switch (status) {
+    case KVX_OK: return "success";
+    case KVX_ERR_NULL: return "a required pointer is NULL";
+    case KVX_ERR_SHAPE: return "element shapes differ or a dimension is out of range";
+    case KVX_ERR_ALIGN: return "a pointer or row size is not 16-byte aligned";
+    case KVX_ERR_LAYOUT: return "unknown layout or num_kv not 1 or 2";
+    case KVX_ERR_RANGE: return "a count, size or pointer is out of range";
+    case KVX_ERR_HIP: return "the HIP runtime reported an error";
+    default: return "unknown kvx status";
+    }
+}
+
+const char *kvx_last_error(void) { return g_last_error.c_str(); }
+
+int kvx_abi_version(void) { return KVX_ABI_VERSION; }
+
+}  // extern "C"

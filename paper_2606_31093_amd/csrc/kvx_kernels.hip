@@ -1,0 +1,380 @@
+// kvx_kernels.hip -- the copy engine of libkvx: HIP kernels for gfx950.
+//
+// One kernel moves the rows named by a batch of request records from a
+// source side to a destination side (Omni-Flow Sec. 4.1.1: layer x page x
+// slice addressing; Sec. 4.1.2: conversion between the paged layout and the
+// flat serialization; Sec. 5.2: slot -> page translation through a table).
+// Nothing is computed on the data: every element moves as raw bytes inside
+// 16-byte vectors, so the kernel is bound by HBM (or the host link when a
+// side is pinned host memory).
+//
+// Work decomposition.  A tile is (request r, page j of the tiling side,
+// layer l); the tiling side is the destination pool for transfer and
+// scatter (each tile then writes one destination page of one layer, and no
+// two tiles write the same bytes) and the source pool for gather.  A
+// persistent grid of workgroups strides over the flat tile index; each
+// workgroup walks the request records in order, keeping a running tile
+// count, so no tile table or scratch memory is needed.
+//
+// Inside a tile the tiling side's rows are a fixed page of one layer.  The
+// other side's rows come from one or more of its pages ("pieces"), whose ids
+// each wavefront loads once into lanes 0..K-1 and broadcasts with a lane
+// shuffle.  When both sides keep the rows of consecutive tokens adjacent
+// (token-major layouts and the flat buffer) and the tile maps onto a single
+// piece, a tile is C contiguous runs on both sides and the copy is a plain
+// vector stream; otherwise each 16-byte vector resolves its row.
+
+#include "kvx_internal.h"
+
+#ifndef KVX_UNROLL_FLAT
+#define KVX_UNROLL_FLAT 8
+#endif
+#ifndef KVX_UNROLL_ROWS
+#define KVX_UNROLL_ROWS 4
+#endif
+#ifndef KVX_NT
+#define KVX_NT 0
+#endif
+#ifndef KVX_BLOCKS_PER_CU
+#define KVX_BLOCKS_PER_CU 0  // 0: as many as fit
+#endif
+
+namespace kvx {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kWave = 64;
+
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ v4u ld16(const char *p) {
+#if KVX_NT
+    return __builtin_nontemporal_load(reinterpret_cast<const v4u *>(p));
+#else
+    return *reinterpret_cast<const v4u *>(p);
+#endif
+}
+
+__device__ __forceinline__ void st16(char *p, v4u v) {
+#if KVX_NT
+    __builtin_nontemporal_store(v, reinterpret_cast<v4u *>(p));
+#else
+    *reinterpret_cast<v4u *>(p) = v;
+#endif
+}
+
+__device__ __forceinline__ void report(const Params &p, uint32_t bits) {
+    if (p.err) atomicOr(p.err, bits);
+}
+
+// A request as one tile walk sees it.
+struct Req {
+    int64_t t_pt_off, o_pt_off;  // table offsets of the tiling / other side
+    int64_t blk;                 // buffer block offset in bytes
+    int64_t tiles;               // tiles this request contributes
+    int32_t t_start, o_start, n;
+    int32_t j0;                  // first tiling-side page (logical)
+};
+
+__device__ __forceinline__ bool block_fits(const Side &b, int64_t off, int32_t n,
+                                           int64_t token_bytes, int32_t e) {
+    if (off < 0 || off > b.cap_bytes / e) return false;
+    const int64_t start = off * e;
+    return (start & 15) == 0 && start + (int64_t)n * token_bytes <= b.cap_bytes;
+}
+
+template <int OP>
+__device__ __forceinline__ bool load_req(const Params &p, int32_t r, Req &q) {
+    const kvx_req &R = p.reqs[r];
+    const int64_t so = R.src_pt_off, dof = R.dst_pt_off, bo = R.buf_off;
+    const int32_t s0 = R.src_start, d0 = R.dst_start, n = R.n_tokens;
+    bool ok = n >= 0 && s0 >= 0 && d0 >= 0 && R.reserved == 0 &&
+              (int64_t)s0 + n <= INT32_MAX && (int64_t)d0 + n <= INT32_MAX;
+    const int64_t token_bytes = (int64_t)p.L * p.C * p.H * p.row_bytes;
+    if (OP == OP_GATHER) ok = ok && d0 == 0 && block_fits(p.dst, bo, n, token_bytes, p.elem_bytes);
+    if (OP == OP_SCATTER) ok = ok && s0 == 0 && block_fits(p.src, bo, n, token_bytes, p.elem_bytes);
+    if (!ok) {
+        q.tiles = 0;
+        return false;
+    }
+    const bool tsrc = OP == OP_GATHER;
+    q.t_pt_off = tsrc ? so : dof;
+    q.o_pt_off = tsrc ? dof : so;
+    q.t_start = tsrc ? s0 : d0;
+    q.o_start = tsrc ? d0 : s0;
+    q.n = n;
+    q.blk = bo * p.elem_bytes;
+    const Side &ts = tsrc ? p.src : p.dst;
+    if (n == 0) {
+        q.tiles = 0;
+        q.j0 = 0;
+        return true;
+    }
+    const int32_t j0 = q.t_start / ts.T;
+    const int32_t j1 = (q.t_start + n - 1) / ts.T;
+    q.j0 = j0;
+    q.tiles = (int64_t)(j1 - j0 + 1) * p.L;
+    return true;
+}
+
+// Plain vector stream over C runs of R vectors each.
+template <int U>
+__device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, int64_t s_sc,
+                                          uint32_t R, int32_t C) {
+    const uint32_t total = R * (uint32_t)C;
+    for (uint32_t k0 = threadIdx.x; k0 < total; k0 += kBlock * U) {
+        v4u v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t k = k0 + u * kBlock;
+            if (k < total) {
+                const uint32_t c = k >= R;
+                const uint32_t w = k - c * R;
+                v[u] = ld16(s + c * s_sc + (int64_t)w * 16);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t k = k0 + u * kBlock;
+            if (k < total) {
+                const uint32_t c = k >= R;
+                const uint32_t w = k - c * R;
+                st16(d + c * d_sc + (int64_t)w * 16, v[u]);
+            }
+        }
+    }
+}
+
+// Everything a tile's row loop needs, fixed for the tile.
+struct Tile {
+    const char *t_base;   // tiling side at (l, page, c = 0, slot = 0, h = 0)
+    int32_t sa, sb;       // tiling-side slots [sa, sb) of this tile
+    int32_t ntok;         // sb - sa
+    // buffer other side
+    const char *o_row0;   // other side at (l, c = 0, token of slot sa, h = 0)
+    int64_t o_sc;         // buffer: bytes between kv components of the block
+    // pool other side
+    int32_t qo_a;         // other-side position of slot sa
+    int32_t jo0;          // other-side logical page of qo_a
+    int32_t pid;          // this lane's piece page id (-1: invalid / unused)
+    int32_t l;
+};
+
+// General row-resolving copy.  Vectors are enumerated in the tiling side's
+// memory order: (c, slot, h, v) when it is token-major, else (c, h, slot, v)
+// over whole pages with the slots outside [sa, sb) masked.
+template <int OP, bool TTHD, int U>
+__device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const Tile &t) {
+    constexpr bool kTileSrc = OP == OP_GATHER;
+    constexpr bool kOtherBuf = OP != OP_TRANSFER;
+    const Side &ts = kTileSrc ? p.src : p.dst;
+    const Side &os = kTileSrc ? p.dst : p.src;
+    const uint32_t H = p.H, vpr = p.vpr, row = p.row_bytes;
+    const uint32_t rows_c = TTHD ? (uint32_t)t.ntok * H : H * (uint32_t)ts.T;
+    const uint32_t total = rows_c * vpr * (uint32_t)p.C;
+    const char *o_l = os.base + (int64_t)t.l * os.s_l;
+    for (uint32_t k0 = threadIdx.x; k0 < total; k0 += kBlock * U) {
+        const char *src[U];
+        char *dst[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const uint32_t kk = k0 + u * kBlock;
+            const uint32_t k = kk < total ? kk : total - 1;
+            bool valid = kk < total;
+            const uint32_t rw = fd_div(p.fd_vpr, k);
+            const uint32_t v = k - rw * vpr;
+            const uint32_t c = rw >= rows_c;
+            const uint32_t rr = rw - c * rows_c;
+            uint32_t h, slot;
+            if (TTHD) {
+                const uint32_t tt = fd_div(p.fd_H, rr);
+                h = rr - tt * H;
+                slot = t.sa + tt;
+            } else {
+                h = fd_div(p.fd_Tt, rr);
+                slot = rr - h * (uint32_t)ts.T;
+                valid = valid && slot >= (uint32_t)t.sa && slot < (uint32_t)t.sb;
+            }
+            const int32_t tt = (int32_t)slot - t.sa;  // token index within the tile
+            const char *ta = t.t_base + c * ts.s_c + (int64_t)slot * ts.s_t +
+                             (int64_t)h * ts.s_h + v * 16;
+            const char *oa;
+            if (kOtherBuf) {
+                oa = t.o_row0 + c * t.o_sc + (int64_t)tt * H * row + h * row + v * 16;
+            } else {
+                const uint32_t qo = (uint32_t)(t.qo_a + tt);
+                const uint32_t jo = fd_div(p.fd_To, qo);
+                const uint32_t so = qo - jo * (uint32_t)os.T;
+                const uint32_t piece = jo - (uint32_t)t.jo0;
+                int32_t pg = __shfl(t.pid, piece < kWave ? piece : kWave - 1, kWave);
+                if (valid && piece >= kWave) {
+                    // More pieces than lanes: resolve this row's page directly.
+                    const int64_t idx = q.o_pt_off + jo;
+                    pg = -1;
+                    if (idx < 0 || idx >= os.pt_len) {
+                        report(p, KVX_DERR_PT_RANGE);
+                    } else {
+                        const int32_t id = os.pt[idx];
+                        if (id < 0 || id >= os.N) report(p, KVX_DERR_SRC_PAGE);
+                        else pg = id;
+                    }
+                }
+                valid = valid && pg >= 0;
+                oa = o_l + (int64_t)pg * os.s_p + c * os.s_c + (int64_t)so * os.s_t +
+                     (int64_t)h * os.s_h + v * 16;
+            }
+            ok[u] = valid;
+            src[u] = kTileSrc ? ta : oa;
+            dst[u] = const_cast<char *>(kTileSrc ? oa : ta);
+        }
+        v4u val[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) val[u] = ld16(src[u]);
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            if (ok[u]) st16(dst[u], val[u]);
+    }
+}
+
+template <int OP, bool TTHD>
+__device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t local) {
+    constexpr bool kTileSrc = OP == OP_GATHER;
+    constexpr bool kOtherBuf = OP != OP_TRANSFER;
+    const Side &ts = kTileSrc ? p.src : p.dst;
+    const Side &os = kTileSrc ? p.dst : p.src;
+
+    Tile t;
+    const int64_t jj = local / p.L;
+    t.l = (int32_t)(local - jj * p.L);
+    const int64_t j = q.j0 + jj;
+    const int64_t page_lo = j * ts.T;
+    const int64_t qa = page_lo > q.t_start ? page_lo : q.t_start;
+    const int64_t q_end = (int64_t)q.t_start + q.n;
+    const int64_t qb = page_lo + ts.T < q_end ? page_lo + ts.T : q_end;
+    t.sa = (int32_t)(qa - page_lo);
+    t.sb = (int32_t)(qb - page_lo);
+    t.ntok = t.sb - t.sa;
+
+    // Tiling-side page (one per tile; a uniform load).
+    const int64_t tidx = q.t_pt_off + j;
+    if (tidx < 0 || tidx >= ts.pt_len) {
+        if (threadIdx.x == 0) report(p, KVX_DERR_PT_RANGE);
+        return;
+    }
+    const int32_t tpage = ts.pt[tidx];
+    if (tpage < 0 || tpage >= ts.N) {
+        if (threadIdx.x == 0) report(p, kTileSrc ? KVX_DERR_SRC_PAGE : KVX_DERR_DST_PAGE);
+        return;
+    }
+    t.t_base = ts.base + (int64_t)t.l * ts.s_l + (int64_t)tpage * ts.s_p;
+
+    const int64_t run_t = (int64_t)t.ntok * p.H * p.vpr;  // vectors per kv run
+    if (kOtherBuf) {
+        const int64_t H_row = (int64_t)p.H * p.row_bytes;
+        const int64_t i0 = qa - q.t_start;
+        t.o_sc = (int64_t)q.n * H_row;
+        t.o_row0 = os.base + q.blk + (int64_t)t.l * p.C * t.o_sc + i0 * H_row;
+        t.pid = -1;
+        t.qo_a = 0;
+        t.jo0 = 0;
+        if (p.flat) {
+            const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
+            if (kTileSrc)
+                copy_runs<KVX_UNROLL_FLAT>(const_cast<char *>(t.o_row0), tb, t.o_sc, ts.s_c,
+                                           (uint32_t)run_t, p.C);
+            else
+                copy_runs<KVX_UNROLL_FLAT>(const_cast<char *>(tb), t.o_row0, ts.s_c, t.o_sc,
+                                           (uint32_t)run_t, p.C);
+            return;
+        }
+    } else {
+        const int32_t delta = q.o_start - q.t_start;
+        t.qo_a = (int32_t)qa + delta;
+        t.jo0 = t.qo_a / os.T;
+        const int32_t jo1 = ((int32_t)qb - 1 + delta) / os.T;
+        const int32_t K = jo1 - t.jo0 + 1;
+        const int32_t lane = threadIdx.x & (kWave - 1);
+        t.pid = -1;
+        if (lane < K) {
+            const int64_t idx = q.o_pt_off + t.jo0 + lane;
+            uint32_t bad = 0;
+            if (idx < 0 || idx >= os.pt_len) {
+                bad = KVX_DERR_PT_RANGE;
+            } else {
+                const int32_t id = os.pt[idx];
+                if (id < 0 || id >= os.N) bad = KVX_DERR_SRC_PAGE;
+                else t.pid = id;
+            }
+            if (bad && threadIdx.x < kWave) report(p, bad);
+        }
+        if (p.flat && K == 1) {
+            const int32_t pg = __builtin_amdgcn_readfirstlane(t.pid);
+            if (pg < 0) return;
+            const int32_t so0 = t.qo_a - t.jo0 * os.T;
+            const char *ob = os.base + (int64_t)t.l * os.s_l + (int64_t)pg * os.s_p +
+                             (int64_t)so0 * os.s_t;
+            const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
+            copy_runs<KVX_UNROLL_FLAT>(const_cast<char *>(tb), ob, ts.s_c, os.s_c,
+                                       (uint32_t)run_t, p.C);
+            return;
+        }
+    }
+    copy_rows<OP, TTHD, KVX_UNROLL_ROWS>(p, q, t);
+}
+
+template <int OP, bool TTHD>
+__global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
+    Req q;
+    int32_t r = -1;
+    int64_t base = 0, cnt = 0;
+    for (int64_t tile = blockIdx.x;; tile += gridDim.x) {
+        while (tile >= base + cnt) {
+            base += cnt;
+            if (++r >= p.n_reqs) return;
+            if (!load_req<OP>(p, r, q) && blockIdx.x == 0 && threadIdx.x == 0)
+                report(p, KVX_DERR_BAD_REQ);
+            cnt = q.tiles;
+        }
+        do_tile<OP, TTHD>(p, q, tile - base);
+    }
+}
+
+typedef void (*KernelFn)(Params);
+
+KernelFn pick(int op, bool tthd) {
+    switch (op) {
+    case OP_TRANSFER:
+        return tthd ? kvx_copy_kernel<OP_TRANSFER, true> : kvx_copy_kernel<OP_TRANSFER, false>;
+    case OP_GATHER:
+        return tthd ? kvx_copy_kernel<OP_GATHER, true> : kvx_copy_kernel<OP_GATHER, false>;
+    default:
+        return tthd ? kvx_copy_kernel<OP_SCATTER, true> : kvx_copy_kernel<OP_SCATTER, false>;
+    }
+}
+
+}  // namespace
+
+// Persistent grid: as many workgroups as the device holds at once.
+int launch(const Params &p, hipStream_t stream) {
+    const bool tthd = (p.op == OP_GATHER ? p.src : p.dst).tok_contig != 0;
+    KernelFn fn = pick(p.op, tthd);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    int cus = 0;
+    e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    int per_cu = KVX_BLOCKS_PER_CU;
+    if (per_cu <= 0) {
+        e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void *>(fn),
+                                                         kBlock, 0);
+        if (e != hipSuccess) return e;
+        if (per_cu < 1) per_cu = 1;
+    }
+    hipLaunchKernelGGL(fn, dim3(cus * per_cu), dim3(kBlock), 0, stream, p);
+    return hipGetLastError();
+}
+
+}  // namespace kvx

@@ -1,0 +1,235 @@
+"""Python binding of libkvx (include/kvx.h): argument marshalling only.
+
+Every step of the copy runs in the library's HIP kernels.  PyTorch supplies
+device memory and the stream: tensors are passed as raw pointers and the
+kernels run on ``torch.cuda.current_stream()`` unless a stream is given.
+The functions keep the C names: ``kvx_transfer``, ``kvx_gather`` and
+``kvx_scatter``.  A missing or unloadable library raises; there is no
+fallback path.
+
+Pool and buffer shapes are duck-typed: a pool shape has integer attributes
+``L C H D T N e`` and a ``layout`` name; a buffer shape has ``L C H D e``
+and ``cap`` (elements).  ``paper_2606_31093_amd.workloads.PoolSpec`` and
+``BufSpec`` fit.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import build_lib
+
+LAYOUTS = {"LPCTHD": 0, "LPCHTD": 1, "PLCTHD": 2, "PLCHTD": 3}
+
+DERR_SRC_PAGE = 1
+DERR_DST_PAGE = 2
+DERR_PT_RANGE = 4
+DERR_BAD_REQ = 8
+
+STATUS = {0: "KVX_OK", -1: "KVX_ERR_NULL", -2: "KVX_ERR_SHAPE", -3: "KVX_ERR_ALIGN",
+          -4: "KVX_ERR_LAYOUT", -5: "KVX_ERR_RANGE", -6: "KVX_ERR_HIP"}
+
+REQ_DTYPE = np.dtype([("src_pt_off", "<i8"), ("dst_pt_off", "<i8"), ("buf_off", "<i8"),
+                      ("src_start", "<i4"), ("dst_start", "<i4"), ("n_tokens", "<i4"),
+                      ("reserved", "<i4")])
+
+
+class Pool(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_void_p), ("num_layers", ctypes.c_int32),
+                ("num_kv", ctypes.c_int32), ("num_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("page_tokens", ctypes.c_int32),
+                ("num_pages", ctypes.c_int32), ("elem_bytes", ctypes.c_int32),
+                ("layout", ctypes.c_int32)]
+
+
+class Buf(ctypes.Structure):
+    _fields_ = [("base", ctypes.c_void_p), ("num_layers", ctypes.c_int32),
+                ("num_kv", ctypes.c_int32), ("num_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("elem_bytes", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("capacity_elems", ctypes.c_int64)]
+
+
+class KvxError(RuntimeError):
+    def __init__(self, status: int, message: str):
+        super().__init__(f"{STATUS.get(status, status)}: {message}")
+        self.status = status
+
+
+_LIB = None
+
+
+def library_path() -> str:
+    return os.environ.get("KVX_LIBRARY", build_lib.LIBRARY)
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded libkvx.so.  Raises if it is missing: build it with
+    ``python -m paper_2606_31093_amd.build_lib`` (or ``__graft_entry__.build()``)."""
+    global _LIB
+    if _LIB is None:
+        path = library_path()
+        if not os.path.exists(path):
+            raise RuntimeError(f"libkvx is not built ({path} missing); run "
+                               "python -m paper_2606_31093_amd.build_lib")
+        L = ctypes.CDLL(path)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        pp, bp = ctypes.POINTER(Pool), ctypes.POINTER(Buf)
+        L.kvx_transfer.argtypes = [pp, pp, vp, i64, vp, i64, vp, i32, vp, vp]
+        L.kvx_gather.argtypes = [pp, bp, vp, i64, vp, i32, vp, vp]
+        L.kvx_scatter.argtypes = [bp, pp, vp, i64, vp, i32, vp, vp]
+        for f in (L.kvx_transfer, L.kvx_gather, L.kvx_scatter):
+            f.restype = ctypes.c_int
+        L.kvx_pool_bytes.argtypes = [pp]
+        L.kvx_pool_bytes.restype = ctypes.c_int64
+        L.kvx_strerror.argtypes = [ctypes.c_int]
+        L.kvx_strerror.restype = ctypes.c_char_p
+        L.kvx_last_error.argtypes = []
+        L.kvx_last_error.restype = ctypes.c_char_p
+        L.kvx_abi_version.argtypes = []
+        L.kvx_abi_version.restype = ctypes.c_int
+        _LIB = L
+    return _LIB
+
+
+# ---------------------------------------------------------------------------
+# descriptors
+# ---------------------------------------------------------------------------
+
+def _ptr(x) -> int | None:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def pool_desc(spec, data=None) -> Pool:
+    """A kvx_pool for a pool shape; ``data`` is a tensor (or raw address)."""
+    return Pool(_ptr(data), spec.L, spec.C, spec.H, spec.D, spec.T, spec.N, spec.e,
+                LAYOUTS[spec.layout] if isinstance(spec.layout, str) else int(spec.layout))
+
+
+def buf_desc(spec, data=None) -> Buf:
+    return Buf(_ptr(data), spec.L, spec.C, spec.H, spec.D, spec.e, 0, spec.cap)
+
+
+def pack_reqs(rows) -> np.ndarray:
+    """(n, 6) int64 rows ``src_pt_off, dst_pt_off, buf_off, src_start,
+    dst_start, n_tokens`` -> kvx_req records (numpy structured array)."""
+    rows = np.asarray(rows, dtype=np.int64).reshape(-1, 6)
+    out = np.zeros(len(rows), dtype=REQ_DTYPE)
+    for i, name in enumerate(("src_pt_off", "dst_pt_off", "buf_off")):
+        out[name] = rows[:, i]
+    for i, name in ((3, "src_start"), (4, "dst_start"), (5, "n_tokens")):
+        col = rows[:, i]
+        if ((col < -2**31) | (col >= 2**31)).any():
+            raise ValueError(f"{name} does not fit int32")
+        out[name] = col
+    return out
+
+
+def device_reqs(rows, device="cuda"):
+    """kvx_req records as a device tensor (bytes)."""
+    import torch
+    recs = pack_reqs(rows)
+    t = torch.from_numpy(recs.view(np.uint8).copy())
+    return t.to(device)
+
+
+def device_table(pt, device="cuda"):
+    import torch
+    a = np.ascontiguousarray(np.asarray(pt if pt is not None else [], dtype=np.int32))
+    return torch.from_numpy(a).to(device)
+
+
+def pool_bytes(spec) -> int:
+    return int(lib().kvx_pool_bytes(ctypes.byref(pool_desc(spec, 0))))
+
+
+# ---------------------------------------------------------------------------
+# entry points
+# ---------------------------------------------------------------------------
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        raise KvxError(status, lib().kvx_last_error().decode())
+
+
+def _n_reqs(reqs) -> int:
+    nbytes = reqs.numel() * reqs.element_size()
+    if nbytes % REQ_DTYPE.itemsize:
+        raise ValueError("reqs must hold whole 40-byte kvx_req records")
+    return nbytes // REQ_DTYPE.itemsize
+
+
+def _len(t) -> int:
+    return 0 if t is None else t.numel()
+
+
+def _need(t, nbytes: int, name: str) -> None:
+    """A tensor argument must hold at least the bytes its descriptor names."""
+    if t is None or isinstance(t, int):
+        return
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{name} holds {have} bytes, its descriptor needs {nbytes}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _pool_nbytes(spec) -> int:
+    return spec.L * spec.C * spec.H * spec.D * spec.T * spec.N * spec.e
+
+
+def kvx_transfer(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, dev_err=None,
+                 stream=None) -> None:
+    """Pool -> pool (see kvx_transfer in include/kvx.h).  ``src_pt`` /
+    ``dst_pt`` are int32 device tensors, ``reqs`` a device tensor from
+    ``device_reqs``, ``dev_err`` an optional int32/uint32 device word."""
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    S, D = pool_desc(src_spec, src), pool_desc(dst_spec, dst)
+    _check(lib().kvx_transfer(ctypes.byref(S), ctypes.byref(D), _ptr(src_pt), _len(src_pt),
+                              _ptr(dst_pt), _len(dst_pt), _ptr(reqs), _n_reqs(reqs),
+                              _ptr(dev_err), _stream(stream)))
+
+
+def kvx_gather(src, src_spec, dst, buf_spec, src_pt, reqs, dev_err=None, stream=None) -> None:
+    """Pool -> flat buffer (see kvx_gather in include/kvx.h)."""
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, buf_spec.cap * buf_spec.e, "dst")
+    S, B = pool_desc(src_spec, src), buf_desc(buf_spec, dst)
+    _check(lib().kvx_gather(ctypes.byref(S), ctypes.byref(B), _ptr(src_pt), _len(src_pt),
+                            _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
+
+
+def kvx_scatter(src, buf_spec, dst, dst_spec, dst_pt, reqs, dev_err=None, stream=None) -> None:
+    """Flat buffer -> pool (see kvx_scatter in include/kvx.h)."""
+    _need(src, buf_spec.cap * buf_spec.e, "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    B, D = buf_desc(buf_spec, src), pool_desc(dst_spec, dst)
+    _check(lib().kvx_scatter(ctypes.byref(B), ctypes.byref(D), _ptr(dst_pt), _len(dst_pt),
+                             _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
+
+
+def kvx_strerror(status: int) -> str:
+    return lib().kvx_strerror(status).decode()
+
+
+def kvx_last_error() -> str:
+    return lib().kvx_last_error().decode()
+
+
+def kvx_abi_version() -> int:
+    return int(lib().kvx_abi_version())

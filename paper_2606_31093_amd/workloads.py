@@ -281,15 +281,21 @@ def random_bytes(nbytes: int, seed: int) -> np.ndarray:
     return np.random.default_rng(seed).integers(0, 256, size=nbytes, dtype=np.uint8)
 
 
+def prefill_words(groups: np.ndarray, tag: int) -> np.ndarray:
+    """Offset-coded destination prefill: the 8-byte group with index g (byte
+    offset 8g in its allocation) holds the little-endian word
+    0x5A<<56 | tag<<48 | g, so any byte can be regenerated from its offset."""
+    g = np.asarray(groups, dtype=np.uint64)
+    w = (np.uint64(0x5A) << np.uint64(56)) | (np.uint64(tag & 0xFF) << np.uint64(48)) | g
+    return w.astype("<u8")
+
+
 def prefill_bytes(nbytes: int, tag: int, start_byte: int = 0) -> np.ndarray:
-    """Offset-coded destination prefill (CPU): the 8-byte group at byte
-    offset 8g holds the little-endian word 0x5A<<56 | tag<<48 | g, so any
-    byte can be regenerated from its offset."""
+    """``prefill_words`` for the byte range [start_byte, start_byte + nbytes)."""
     if nbytes % 8 or start_byte % 8:
         raise ValueError("prefill covers whole 8-byte groups")
     g = np.arange(start_byte // 8, (start_byte + nbytes) // 8, dtype=np.uint64)
-    w = (np.uint64(0x5A) << np.uint64(56)) | (np.uint64(tag & 0xFF) << np.uint64(48)) | g
-    return w.astype("<u8").view(np.uint8)
+    return prefill_words(g, tag).view(np.uint8)
 
 
 def fill_normal_bf16_(t, seed: int, chunk_elems: int = 1 << 28) -> None:
@@ -325,3 +331,34 @@ def fill_prefill_(t, tag: int, chunk_groups: int = 1 << 27) -> None:
     for s in range(0, w.numel(), chunk_groups):
         e = min(w.numel(), s + chunk_groups)
         w[s:e].copy_(torch.arange(s, e, device=t.device, dtype=torch.int64) | hi)
+
+
+# --------------------------------------------------------------------------
+# device placement (torch is used for memory only)
+# --------------------------------------------------------------------------
+
+def alloc_side(spec, device="cuda", pinned=False):
+    """Bytes for one side: device memory, or pinned host memory."""
+    import torch
+    if pinned:
+        return torch.empty(spec.nbytes, dtype=torch.uint8, pin_memory=True)
+    return torch.empty(spec.nbytes, dtype=torch.uint8, device=device)
+
+
+def value_side(wl: Workload) -> str:
+    """The side that holds the source values (the first step's source)."""
+    return wl.steps[0].src
+
+
+def init_sides_(wl: Workload, tensors: dict) -> None:
+    """Source values into the value side, offset-coded prefill elsewhere."""
+    vs = value_side(wl)
+    for name, t in tensors.items():
+        spec = wl.sides[name]
+        if name == vs:
+            if spec.e == 2:
+                fill_normal_bf16_(t, wl.value_seed)
+            else:
+                fill_random_bytes_(t, wl.value_seed)
+        else:
+            fill_prefill_(t, wl.prefill_tag)

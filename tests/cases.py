@@ -1,0 +1,88 @@
+"""Seeded small cases for parity checks: random page tables, shifted and
+ragged ranges, shared source pages, every layout pair and page-size pair.
+
+A case is a ``Workload`` (see paper_2606_31093_amd.workloads) so the same
+runner drives the oracle and the HIP path.
+"""
+from __future__ import annotations
+
+import itertools
+
+import numpy as np
+
+from paper_2606_31093_amd.workloads import LAYOUTS, BufSpec, PoolSpec, Step, Workload
+
+
+def _cdiv(a, b):
+    return -(-a // b)
+
+
+def transfer_case(ls, ld, Ts, Td, seed, *, e=2, D=8, L=2, C=2, H=3, spec=None,
+                  extra_pages=8) -> Workload:
+    """Pool -> pool.  ``spec`` lists (src_start, dst_start, n, share) per
+    request; share names an earlier request whose source pages it reuses."""
+    rng = np.random.default_rng(seed)
+    if spec is None:
+        spec = [
+            (Ts // 2 + 1, Td - 1, 3 * Ts + 1, None),   # both starts mid-page, ragged end
+            (0, 1, 2 * Ts - 1, 0),                     # shares request 0's source pages
+            (Ts - 1, 2 * Td - 1, 1, None),             # one token
+            (0, 0, 0, None),                           # empty
+            (0, 0, min(Td, 2 * Ts), None),             # page-aligned
+        ]
+    ks = [_cdiv(s0 + n, Ts) for s0, _d0, n, share in spec if share is None]
+    kd = [_cdiv(d0 + n, Td) for _s0, d0, n, _share in spec]
+    S = PoolSpec(L, C, H, D, T=Ts, N=sum(ks) + extra_pages, e=e, layout=ls)
+    Dp = PoolSpec(L, C, H, D, T=Td, N=sum(kd) + extra_pages, e=e, layout=ld)
+    sperm, dperm = rng.permutation(S.N).astype(np.int32), rng.permutation(Dp.N).astype(np.int32)
+    src_pt, dst_pt, rows, src_offs = [], [], [], []
+    for s0, d0, n, share in spec:
+        k_s, k_d = _cdiv(s0 + n, Ts), _cdiv(d0 + n, Td)
+        so = src_offs[share] if share is not None else len(src_pt)
+        if share is None:
+            src_pt.extend(sperm[len(src_pt): len(src_pt) + k_s])
+        src_offs.append(so)
+        rows.append([so, len(dst_pt), 0, s0, d0, n])
+        dst_pt.extend(dperm[len(dst_pt): len(dst_pt) + k_d])
+    step = Step("transfer", "A", "B", np.asarray(src_pt, np.int32), np.asarray(dst_pt, np.int32),
+                np.asarray(rows, np.int64).reshape(-1, 6))
+    return Workload(0, f"transfer {ls}/T{Ts} -> {ld}/T{Td} e{e} D{D} L{L} C{C} H{H}",
+                    {"A": S, "B": Dp}, [step], value_seed=seed, prefill_tag=seed & 0xFF)
+
+
+def gather_scatter_case(layout, T, e, D, seed, *, L=3, C=2, H=2, pinned=False) -> Workload:
+    """Pool -> flat buffer -> a second pool of the same shape on other pages."""
+    rng = np.random.default_rng(seed)
+    ns = [5 * T // 2 + 1, 0, 1, 2 * T]
+    starts = [T // 2 + 1, 0, T - 1, 0]
+    align = 16 // e
+    blocks, off = [], 0
+    for n in ns:
+        blocks.append(off)
+        off += _cdiv(L * C * n * H * D, align) * align + align    # gaps between blocks
+    B = BufSpec(L, C, H, D, e, cap=off)
+    need = sum(_cdiv(s0 + n, T) for n, s0 in zip(ns, starts))
+    S = PoolSpec(L, C, H, D, T=T, N=need + 5, e=e, layout=layout)
+    perm = rng.permutation(S.N).astype(np.int32)
+    pt, pos, g_rows = [], 0, []
+    for n, s0, bo in zip(ns, starts, blocks):
+        k = _cdiv(s0 + n, T)
+        g_rows.append([pos, 0, bo, s0, 0, n])
+        pt.extend(perm[pos: pos + k])
+        pos += k
+    s_rows = [[0, r[0], r[2], 0, r[3], r[5]] for r in g_rows]
+    dperm = rng.permutation(S.N).astype(np.int32)[: len(pt)]
+    steps = [Step("gather", "A", "buf", np.asarray(pt, np.int32), None, np.asarray(g_rows, np.int64)),
+             Step("scatter", "buf", "B", None, dperm, np.asarray(s_rows, np.int64))]
+    return Workload(0, f"gather/scatter {layout} T{T} e{e} D{D}", {"A": S, "buf": B, "B": S},
+                    steps, value_seed=seed, prefill_tag=seed & 0xFF,
+                    host_sides=("buf",) if pinned else ())
+
+
+T_PAIRS = [(16, 64), (32, 8), (4, 4), (1, 16), (8, 1), (64, 64), (2, 128)]
+
+
+def layout_matrix():
+    """Every (source layout, destination layout, T_src, T_dst)."""
+    for (ls, ld), (Ts, Td) in itertools.product(itertools.product(LAYOUTS, LAYOUTS), T_PAIRS):
+        yield ls, ld, Ts, Td

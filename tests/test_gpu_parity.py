@@ -1,0 +1,200 @@
+"""HIP path vs the CPU oracle, bit for bit, at sizes the oracle finishes in
+seconds: the tiny workload, shrunken versions of the four large ones, every
+layout pair and page-size pair, every element width, pinned host buffers,
+tiles spanning more source pages than a wavefront has lanes, and the
+documented error behaviour."""
+import numpy as np
+import pytest
+
+import cases
+from paper_2606_31093_amd.workloads import PoolSpec, BufSpec, Step, Workload, config
+from runner import assert_same, initial_bytes, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_31093_amd import kvx
+    kvx.lib()    # raises if libkvx.so is missing: no fallback
+
+
+def check(wl, raw_reqs=None, oracle_reqs=None):
+    init = initial_bytes(wl)
+    want, werr = run_oracle(wl, init, oracle_reqs)
+    got, gerr = run_gpu(wl, init, raw_reqs)
+    assert gerr == werr, f"{wl.title}: device error bits {gerr}, oracle {werr}"
+    assert_same(got, want, wl.title)
+    return got, gerr
+
+
+def test_config1_tiny():
+    check(config(1))
+
+
+@pytest.mark.parametrize("k", [2, 3, 4, 5])
+def test_small_configs(k):
+    check(config(k, small=True))
+
+
+@pytest.mark.parametrize("ls,ld,Ts,Td", list(cases.layout_matrix()),
+                         ids=lambda v: str(v))
+def test_layout_matrix(ls, ld, Ts, Td):
+    check(cases.transfer_case(ls, ld, Ts, Td, seed=hash((ls, ld, Ts, Td)) & 0xFFFF))
+
+
+@pytest.mark.parametrize("e,D,C,H", [(1, 16, 2, 3), (2, 8, 2, 3), (4, 4, 1, 5), (8, 2, 2, 1),
+                                     (8, 8, 2, 2), (1, 48, 1, 1), (2, 576, 1, 1),
+                                     (2, 128, 2, 8), (4, 12, 2, 2)])
+@pytest.mark.parametrize("ls,ld", [("LPCTHD", "LPCTHD"), ("LPCTHD", "PLCHTD"),
+                                   ("LPCHTD", "PLCTHD")])
+def test_element_widths(e, D, C, H, ls, ld):
+    check(cases.transfer_case(ls, ld, 4, 8, seed=e * 1000 + D, e=e, D=D, C=C, H=H))
+
+
+@pytest.mark.parametrize("layout", ["LPCTHD", "LPCHTD", "PLCTHD", "PLCHTD"])
+@pytest.mark.parametrize("T,e,D", [(16, 2, 64), (4, 2, 8), (8, 1, 16), (2, 4, 12), (1, 8, 2),
+                                   (64, 2, 576)])
+@pytest.mark.parametrize("pinned", [False, True], ids=["device_buf", "pinned_host_buf"])
+def test_gather_scatter(layout, T, e, D, pinned):
+    check(cases.gather_scatter_case(layout, T, e, D, seed=T * 31 + e * 7 + D, pinned=pinned))
+
+
+@pytest.mark.parametrize("ls,ld", [("LPCTHD", "LPCTHD"), ("LPCTHD", "PLCHTD"),
+                                   ("PLCHTD", "LPCHTD")])
+def test_more_pieces_than_lanes(ls, ld):
+    """One destination page of 128 tokens fed by 1-token source pages: up to
+    128 source pages per tile, beyond the 64 a wavefront broadcasts."""
+    check(cases.transfer_case(ls, ld, 1, 128, seed=77, H=2,
+                              spec=[(3, 5, 200, None), (0, 0, 128, None), (1, 0, 64, None)]))
+
+
+def test_many_requests_and_empty_ones():
+    spec = [((7 * i) % 13, (5 * i) % 11, (i * 37) % 90 if i % 4 else 0, None) for i in range(60)]
+    check(cases.transfer_case("LPCTHD", "PLCHTD", 16, 32, seed=5, H=2, D=64, spec=spec))
+
+
+# ---------------------------------------------------------------------------
+# error behaviour
+# ---------------------------------------------------------------------------
+
+def _err_wl(src_pt, dst_pt, rows, N=4, T=4):
+    S = PoolSpec(1, 2, 1, 8, T=T, N=N, e=2, layout="LPCTHD")
+    return Workload(0, f"errors {rows}", {"A": S, "B": S},
+                    [Step("transfer", "A", "B", np.asarray(src_pt, np.int32),
+                          np.asarray(dst_pt, np.int32), np.asarray(rows, np.int64).reshape(-1, 6))],
+                    value_seed=3, prefill_tag=9)
+
+
+@pytest.mark.parametrize("src_pt,dst_pt,row,bits", [
+    ([0, 4], [0, 1], [0, 0, 0, 0, 0, 8], 1),          # source page id == N
+    ([0, 1], [-1, 1], [0, 0, 0, 0, 0, 8], 2),         # negative destination page id
+    ([7, 1], [-1, 1], [0, 0, 0, 0, 0, 4], 2),         # both bad: destination first
+    ([7, 1], [0, 1], [0, 0, 0, 0, 0, 4], 1),
+    ([0], [0, 1], [0, 0, 0, 0, 0, 8], 4),             # source table too short
+    ([0, 1], [0, 1], [0, 1, 0, 0, 0, 8], 4),          # destination table too short
+    ([0, 1], [0, 1], [0, 0, 0, 0, 0, -1], 8),         # negative count
+    ([0, 1], [0, 1], [0, 0, 0, -1, 0, 2], 8),         # negative start
+    ([0, 1], [0, 1], [0, 0, 0, 2**31 - 2, 0, 3], 8),  # end beyond 2^31 - 1
+    ([0, 1, 2, 3], [2, 0, 1, 3], [0, 0, 0, 3, 6, 9], 0),
+])
+def test_device_errors(src_pt, dst_pt, row, bits):
+    _, errs = check(_err_wl(src_pt, dst_pt, [row, [0, 0, 0, 0, 0, 2]]))
+    assert errs == [bits]
+
+
+def test_buffer_record_errors():
+    """Buffer-side start must be 0; the block must be 16-byte aligned and
+    inside the buffer (ending exactly at its end is fine)."""
+    S = PoolSpec(1, 2, 1, 8, T=4, N=4, e=2, layout="LPCTHD")
+    n = 3
+    B = BufSpec(1, 2, 1, 8, 2, cap=2 * n * 8 + 8)
+    for row, bits in (([0, 0, 8, 0, 0, n], 0), ([0, 0, 0, 0, 0, n], 0), ([0, 0, 16, 0, 0, n], 8),
+                      ([0, 0, 4, 0, 0, n], 8), ([0, 0, -8, 0, 0, n], 8), ([0, 0, 0, 0, 1, n], 8)):
+        wl = Workload(0, f"gather {row}", {"A": S, "buf": B},
+                      [Step("gather", "A", "buf", np.asarray([0, 1], np.int32), None,
+                            np.asarray([row], np.int64))], value_seed=1, prefill_tag=2)
+        _, errs = check(wl)
+        assert errs == [bits]
+    for row, bits in (([0, 0, 8, 0, 0, n], 0), ([0, 0, 16, 0, 0, n], 8), ([0, 0, 0, 2, 0, n], 8)):
+        wl = Workload(0, f"scatter {row}", {"buf": B, "B": S},
+                      [Step("scatter", "buf", "B", None, np.asarray([2, 3], np.int32),
+                            np.asarray([row], np.int64))], value_seed=1, prefill_tag=2)
+        _, errs = check(wl)
+        assert errs == [bits]
+
+
+def test_reserved_field_must_be_zero():
+    """A record whose reserved word is not 0 is skipped with BAD_REQ (a rule
+    of the C record format, so the oracle sees the record as absent)."""
+    from paper_2606_31093_amd import kvx
+    wl = _err_wl([0, 1], [2, 3], [[0, 0, 0, 0, 0, 8], [0, 0, 0, 0, 0, 3]])
+    recs = kvx.pack_reqs(wl.steps[0].reqs)
+    recs["reserved"][0] = 1
+    init = initial_bytes(wl)
+    want, werr = run_oracle(wl, init, [wl.steps[0].reqs[1:]])
+    got, gerr = run_gpu(wl, init, [recs])
+    assert werr == [0] and gerr == [8]
+    assert_same(got, want, wl.title)
+
+
+def test_max_position():
+    T = 1 << 16
+    S = PoolSpec(1, 1, 1, 8, T=T, N=1, e=2, layout="LPCTHD")
+    B = BufSpec(1, 1, 1, 8, 2, cap=5 * 8)
+    wl = Workload(0, "max position", {"A": S, "buf": B},
+                  [Step("gather", "A", "buf", np.zeros(32768, np.int32), None,
+                        np.asarray([[0, 0, 0, 2**31 - 6, 0, 5]], np.int64))],
+                  value_seed=4, prefill_tag=4)
+    _, errs = check(wl)
+    assert errs == [0]
+
+
+def test_zero_records_enqueue_nothing():
+    import torch
+    from paper_2606_31093_amd import kvx
+    S = PoolSpec(1, 2, 1, 8, T=4, N=4, e=2, layout="LPCTHD")
+    a = torch.zeros(S.nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.ones(S.nbytes, dtype=torch.uint8, device="cuda")
+    reqs = torch.empty(0, dtype=torch.uint8, device="cuda")
+    kvx.kvx_transfer(a, S, b, S, None, None, reqs)
+    torch.cuda.synchronize()
+    assert bool((b == 1).all())
+
+
+def test_side_stream():
+    """Work runs on the stream passed in, ordered with other work there."""
+    import torch
+    from paper_2606_31093_amd import kvx
+    wl = config(2, small=True)
+    init = initial_bytes(wl)
+    want, _ = run_oracle(wl, init)
+    st = wl.steps[0]
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        a = torch.from_numpy(init["A"]).to("cuda")
+        b = torch.from_numpy(init["B"]).to("cuda")
+        kvx.kvx_transfer(a, wl.sides["A"], b, wl.sides["B"], kvx.device_table(st.src_pt),
+                         kvx.device_table(st.dst_pt), kvx.device_reqs(st.reqs), stream=s)
+        got = b.cpu().numpy()
+    assert np.array_equal(got, want["B"])
+
+
+def test_host_validation_errors_raise():
+    import torch
+    from paper_2606_31093_amd import kvx
+    S = PoolSpec(1, 2, 1, 8, T=4, N=4, e=2, layout="LPCTHD")
+    a = torch.zeros(S.nbytes, dtype=torch.uint8, device="cuda")
+    reqs = kvx.device_reqs([[0, 0, 0, 0, 0, 1]])
+    pt = kvx.device_table([0])
+    host = torch.zeros(S.nbytes, dtype=torch.uint8)   # pageable host memory
+    with pytest.raises(kvx.KvxError) as ei:
+        kvx.kvx_transfer(a, S, host, S, pt, pt, reqs)
+    assert ei.value.status == -5
+    big = torch.zeros(S.nbytes + 16, dtype=torch.uint8, device="cuda")
+    with pytest.raises(kvx.KvxError) as ei:
+        kvx.kvx_transfer(a, S, big[1:1 + S.nbytes], S, pt, pt, reqs)   # misaligned base
+    assert ei.value.status == -3
