@@ -227,6 +227,23 @@ def main() -> int:
             launch(d)
         torch.cuda.synchronize()
 
+    if not args.no_memcpy and host_leg:
+        # hipMemcpyAsync between the same pinned buffer and HBM, per direction
+        hs = wl.host_sides[0]
+        host = mem[hs]
+        other = [n for n in wl.sides if n != hs][0]
+        nb = min(host.numel(), mem[other].numel())
+        for name, fn in (("hip_memcpy_d2h_GBps", lambda: host[:nb].copy_(mem[other][:nb], non_blocking=True)),
+                         ("hip_memcpy_h2d_GBps", lambda: mem[other][:nb].copy_(host[:nb], non_blocking=True))):
+            fn()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            context[name] = round(nb / (e0.elapsed_time(e1) / 1e3) / 1e9, 2)
+
     cpu = None
     if args.cpu_layers > 0 and not host_leg:
         from oracle import layer_check

@@ -85,3 +85,27 @@ def check_transfer_layer(src_t, S, dst_t, D, step, l: int, tag: int) -> LayerRes
     dt = time.perf_counter() - t0
     moved = 2 * int(step.reqs[:, 5].sum()) * S.C * S.H * S.D * S.e
     return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved)
+
+
+def gather_scatter_layer(pool_before: np.ndarray, S, buf_t, B, pool_after: np.ndarray,
+                         gather, scatter, l: int) -> tuple[bool, bool]:
+    """Layer l of a gather (pool -> flat buffer) followed by a scatter (flat
+    buffer -> the same pool): the oracle gathers the layer from the pool as
+    it was before, compares with the device buffer, scatters into a copy of
+    the pool layer and compares with the device pool afterwards."""
+    s1 = one_layer(S)
+    blocks = [(int(r[2]), int(r[5])) for r in gather.reqs]
+    got_buf, offs = buf_layer(buf_t, B, l, blocks)
+    b1 = dataclasses.replace(B, L=1, cap=got_buf.nbytes // B.e)
+    g_rows = gather.reqs.copy()
+    g_rows[:, 2] = offs
+    want_buf = np.zeros_like(got_buf)
+    O = kvx_oracle.default()
+    ok_g = O.gather(pool_before, s1, want_buf, b1, gather.src_pt, g_rows) == 0 and \
+        np.array_equal(got_buf, want_buf)
+    s_rows = scatter.reqs.copy()
+    s_rows[:, 2] = offs
+    want_pool = pool_before.copy()
+    ok_s = O.scatter(want_buf, b1, want_pool, s1, scatter.dst_pt, s_rows) == 0 and \
+        np.array_equal(pool_after, want_pool)
+    return ok_g, ok_s

@@ -1,0 +1,229 @@
+"""The C-ABI boundary on the CPU: the library loads and exports every
+function include/kvx.h declares; the Python structures match the C layout;
+host-side validation returns the documented status for each kind of bad
+argument without touching a GPU; the launch-constant division is exact."""
+import ctypes
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+from paper_2606_31093_amd import build_lib, kvx
+from paper_2606_31093_amd.workloads import BufSpec, PoolSpec
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvx.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if build_lib.is_stale():
+        build_lib.build()
+    return kvx.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w \*]*?\b(kvx_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for n in ("kvx_transfer", "kvx_gather", "kvx_scatter", "kvx_pool_bytes", "kvx_strerror",
+              "kvx_last_error", "kvx_abi_version"):
+        assert n in names
+
+
+def test_library_exports_every_declared_function(lib):
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in kvx.h but not exported"
+    out = subprocess.run(["nm", "-D", "--defined-only", build_lib.LIBRARY], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\b(kvx_\w+)$", out, flags=re.M))
+    assert set(declared_functions()) <= exported
+
+
+def test_abi_version(lib):
+    m = re.search(r"#define KVX_ABI_VERSION (\d+)", open(HEADER).read())
+    assert kvx.kvx_abi_version() == int(m.group(1))
+
+
+def test_struct_layout_matches_c(tmp_path):
+    """sizeof/offsetof from a C compiler against the ctypes/numpy mirrors."""
+    src = tmp_path / "layout.c"
+    src.write_text(r'''
+#include <stddef.h>
+#include <stdio.h>
+#include "kvx.h"
+#define F(T, f) printf(#T "." #f " %zu\n", offsetof(T, f))
+int main(void) {
+  printf("kvx_pool %zu\nkvx_buf %zu\nkvx_req %zu\n", sizeof(kvx_pool), sizeof(kvx_buf), sizeof(kvx_req));
+  F(kvx_pool, base); F(kvx_pool, num_layers); F(kvx_pool, num_kv); F(kvx_pool, num_heads);
+  F(kvx_pool, head_dim); F(kvx_pool, page_tokens); F(kvx_pool, num_pages); F(kvx_pool, elem_bytes);
+  F(kvx_pool, layout);
+  F(kvx_buf, base); F(kvx_buf, num_layers); F(kvx_buf, num_kv); F(kvx_buf, num_heads);
+  F(kvx_buf, head_dim); F(kvx_buf, elem_bytes); F(kvx_buf, reserved); F(kvx_buf, capacity_elems);
+  F(kvx_req, src_pt_off); F(kvx_req, dst_pt_off); F(kvx_req, buf_off); F(kvx_req, src_start);
+  F(kvx_req, dst_start); F(kvx_req, n_tokens); F(kvx_req, reserved);
+  return 0;
+}''')
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), "-o", str(exe), str(src)],
+                   check=True)
+    got = dict(line.rsplit(" ", 1) for line in
+               subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.split("\n")
+               if line)
+    got = {k: int(v) for k, v in got.items()}
+    assert got["kvx_pool"] == ctypes.sizeof(kvx.Pool)
+    assert got["kvx_buf"] == ctypes.sizeof(kvx.Buf)
+    assert got["kvx_req"] == kvx.REQ_DTYPE.itemsize
+    for name, _ in kvx.Pool._fields_:
+        assert got[f"kvx_pool.{name}"] == getattr(kvx.Pool, name).offset
+    for name, _ in kvx.Buf._fields_:
+        assert got[f"kvx_buf.{name}"] == getattr(kvx.Buf, name).offset
+    for name in kvx.REQ_DTYPE.names:
+        assert got[f"kvx_req.{name}"] == kvx.REQ_DTYPE.fields[name][1]
+
+
+def test_strerror(lib):
+    for status, text in ((0, "success"), (-1, "NULL"), (-2, "shape"), (-3, "aligned"),
+                         (-4, "layout"), (-5, "range"), (-6, "HIP"), (-99, "unknown")):
+        assert text.lower() in kvx.kvx_strerror(status).lower()
+
+
+def test_pool_bytes(lib):
+    s = PoolSpec(36, 2, 8, 128, T=64, N=4096, e=2, layout="LPCTHD")
+    assert kvx.pool_bytes(s) == s.nbytes == 36 * 2**30
+    assert kvx.pool_bytes(PoolSpec(1, 3, 1, 8, T=4, N=1)) == -1        # num_kv 3
+    assert kvx.pool_bytes(PoolSpec(1, 1, 1, 7, T=4, N=1)) == -1        # 14-byte rows
+
+
+FAKE = 1 << 20      # a 16-byte aligned address that is never dereferenced
+
+
+def _call_transfer(S, D, n_reqs=1, src_pt_len=1, dst_pt_len=1, reqs=FAKE, src_pt=FAKE,
+                   dst_pt=FAKE, err=None, sbase=FAKE, dbase=FAKE):
+    L = kvx.lib()
+    sp = kvx.pool_desc(S, sbase)
+    dp = kvx.pool_desc(D, dbase)
+    return L.kvx_transfer(ctypes.byref(sp), ctypes.byref(dp), src_pt, src_pt_len, dst_pt, dst_pt_len,
+                          reqs, n_reqs, err, None)
+
+
+GOOD = PoolSpec(2, 2, 4, 64, T=16, N=8, e=2, layout="LPCTHD")
+
+
+@pytest.mark.parametrize("S,D,kw,status", [
+    (GOOD, PoolSpec(2, 2, 4, 64, T=16, N=8, e=2, layout="PLCHTD"), dict(n_reqs=0), 0),
+    (GOOD, PoolSpec(3, 2, 4, 64, T=16, N=8, e=2), {}, -2),             # layers differ
+    (GOOD, PoolSpec(2, 2, 4, 32, T=16, N=8, e=2), {}, -2),             # head_dim differs
+    (GOOD, PoolSpec(2, 2, 4, 64, T=16, N=8, e=4), {}, -2),             # elem_bytes differs
+    (PoolSpec(2, 3, 4, 64, T=16, N=8), PoolSpec(2, 3, 4, 64, T=16, N=8), {}, -4),   # num_kv 3
+    (PoolSpec(2, 2, 4, 64, T=16, N=8, layout=7), GOOD, {}, -4),        # layout 7
+    (PoolSpec(2, 2, 4, 4, T=16, N=8), PoolSpec(2, 2, 4, 4, T=16, N=8), {}, -3),     # 8-byte rows
+    (PoolSpec(2, 2, 4, 64, T=16, N=8, e=3), PoolSpec(2, 2, 4, 64, T=16, N=8, e=3), {}, -2),
+    (PoolSpec(2, 2, 4, 64, T=0, N=8), GOOD, {}, -2),                   # page_tokens 0
+    (PoolSpec(2, 2, 4, 64, T=(1 << 20) + 1, N=8), GOOD, {}, -2),       # page_tokens too large
+    (PoolSpec(2, 2, 4, 64, T=16, N=0), GOOD, {}, -2),                  # no pages
+    (PoolSpec(0, 2, 4, 64, T=16, N=8), PoolSpec(0, 2, 4, 64, T=16, N=8), {}, -2),
+    (GOOD, GOOD, dict(sbase=FAKE + 8), -3),                             # misaligned base
+    (GOOD, GOOD, dict(dbase=0), -1),                                   # NULL base
+    (GOOD, GOOD, dict(reqs=None), -1),                                 # NULL records
+    (GOOD, GOOD, dict(reqs=FAKE + 4), -3),                             # misaligned records
+    (GOOD, GOOD, dict(n_reqs=-1), -5),
+    (GOOD, GOOD, dict(n_reqs=65537), -5),
+    (GOOD, GOOD, dict(src_pt_len=-1), -5),
+    (GOOD, GOOD, dict(src_pt=None), -1),                               # NULL table with entries
+    (GOOD, GOOD, dict(dst_pt=FAKE + 2), -3),                           # misaligned table
+    (GOOD, GOOD, dict(err=FAKE + 2), -3),                              # misaligned error word
+])
+def test_transfer_host_validation(lib, S, D, kw, status):
+    assert _call_transfer(S, D, **kw) == status
+    if status:
+        assert kvx.kvx_last_error() != ""
+    else:
+        assert kvx.kvx_last_error() == ""
+
+
+def test_gather_scatter_host_validation(lib):
+    L = kvx.lib()
+    sp = kvx.pool_desc(GOOD, FAKE)
+    b = BufSpec(2, 2, 4, 64, 2, cap=1 << 16)
+    bd = kvx.buf_desc(b, FAKE)
+    assert L.kvx_gather(ctypes.byref(sp), ctypes.byref(bd), FAKE, 1, FAKE, 0, None, None) == 0
+    assert L.kvx_scatter(ctypes.byref(bd), ctypes.byref(sp), FAKE, 1, FAKE, 0, None, None) == 0
+    bad = kvx.buf_desc(BufSpec(2, 2, 4, 64, 2, cap=-1), FAKE)
+    assert L.kvx_gather(ctypes.byref(sp), ctypes.byref(bad), FAKE, 1, FAKE, 1, None, None) == -5
+    bd.reserved = 1
+    assert L.kvx_scatter(ctypes.byref(bd), ctypes.byref(sp), FAKE, 1, FAKE, 1, None, None) == -5
+    bd.reserved = 0
+    wrong = kvx.buf_desc(BufSpec(2, 2, 8, 64, 2, cap=1 << 16), FAKE)
+    assert L.kvx_gather(ctypes.byref(sp), ctypes.byref(wrong), FAKE, 1, FAKE, 1, None, None) == -2
+    assert L.kvx_gather(None, ctypes.byref(bd), FAKE, 1, FAKE, 1, None, None) == -1
+    assert L.kvx_scatter(ctypes.byref(bd), None, FAKE, 1, FAKE, 1, None, None) == -1
+
+
+def test_last_error_is_per_call(lib):
+    assert _call_transfer(GOOD, GOOD, n_reqs=-1) == -5
+    assert "n_reqs" in kvx.kvx_last_error()
+    assert _call_transfer(GOOD, GOOD, n_reqs=0) == 0
+    assert kvx.kvx_last_error() == ""
+
+
+def test_pack_reqs_round_trip():
+    rows = np.array([[1, 2, 3, 4, 5, 6], [7, 8, 9, 10, 11, 12]], np.int64)
+    rec = kvx.pack_reqs(rows)
+    assert rec.itemsize == 40 and (rec["reserved"] == 0).all()
+    back = np.stack([rec[n].astype(np.int64) for n in ("src_pt_off", "dst_pt_off", "buf_off",
+                                                       "src_start", "dst_start", "n_tokens")], 1)
+    assert (back == rows).all()
+    with pytest.raises(ValueError):
+        kvx.pack_reqs([[0, 0, 0, 2**31, 0, 1]])
+
+
+def test_fastdiv_exact(tmp_path):
+    """The multiply-shift division used for launch constants is exact for
+    every dividend below 2^31: exhaustive over small divisors and dividends,
+    and on edges and random values for large ones."""
+    src = tmp_path / "fd.cpp"
+    src.write_text(r'''
+#include <cstdio>
+#include <cstdint>
+#include <random>
+#include "kvx_internal.h"
+int main() {
+  std::mt19937_64 rng(1234);
+  long bad = 0, checked = 0;
+  auto check = [&](uint32_t d, uint32_t n) {
+    kvx::FastDiv f = kvx::make_fastdiv(d);
+    ++checked;
+    if (kvx::fd_div(f, n) != n / d) { if (bad < 5) printf("d=%u n=%u\n", d, n); ++bad; }
+  };
+  for (uint32_t d = 1; d < 1200; ++d)
+    for (uint32_t n = 0; n < 70000; ++n) check(d, n);
+  const uint32_t top = 0x7fffffffu;
+  for (int i = 0; i < 200000; ++i) {
+    uint32_t d = 1 + (uint32_t)(rng() % top);
+    if (i % 3 == 0) d = 1 + (uint32_t)(rng() % 70000);
+    uint32_t n = (uint32_t)(rng() % (uint64_t(top) + 1));
+    check(d, n);
+    uint64_t q = n / d;
+    for (int64_t e = -1; e <= 1; ++e) { int64_t m = (int64_t)(q * d) + e; if (m >= 0 && m <= top) check(d, (uint32_t)m); }
+    check(d, top);
+  }
+  for (uint32_t s = 0; s < 31; ++s) for (int e = -1; e <= 1; ++e) {
+    int64_t d = ((int64_t)1 << s) + e; if (d < 1 || d > top) continue;
+    for (uint32_t n : {0u, 1u, (uint32_t)d - 1, (uint32_t)d, top, top - 1}) check((uint32_t)d, n);
+  }
+  printf("checked %ld bad %ld\n", checked, bad);
+  return bad != 0;
+}''')
+    exe = tmp_path / "fd"
+    cmd = [build_lib.hipcc(), "-O2", "-std=c++17", "-I", os.path.join(ROOT, "include"),
+           "-I", build_lib.CSRC, "-o", str(exe), str(src)]
+    subprocess.run(cmd, check=True, capture_output=True)
+    r = subprocess.run([str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stdout

@@ -1,0 +1,92 @@
+"""Full-size workloads on the GPU, in the launch configuration bench.py
+times, checked against the CPU oracle one layer at a time (layers never mix:
+a layer slice of a pool is a one-layer pool of the same layout)."""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_31093_amd import kvx
+    kvx.lib()
+    return torch
+
+
+def _setup(torch, k):
+    from paper_2606_31093_amd import kvx, workloads
+    wl = workloads.config(k)
+    dev = torch.device("cuda", 0)
+    mem = {n: workloads.alloc_side(s, dev, pinned=n in wl.host_sides) for n, s in wl.sides.items()}
+    workloads.init_sides_(wl, mem)
+    dsteps = [dict(st=st,
+                   spt=kvx.device_table(st.src_pt) if st.src_pt is not None else None,
+                   dpt=kvx.device_table(st.dst_pt) if st.dst_pt is not None else None,
+                   reqs=kvx.device_reqs(st.reqs)) for st in wl.steps]
+    torch.cuda.synchronize()
+    return wl, mem, dsteps
+
+
+def _run(torch, wl, mem, d):
+    from paper_2606_31093_amd import kvx
+    st = d["st"]
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    S, D = wl.sides[st.src], wl.sides[st.dst]
+    if st.op == "transfer":
+        kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"], err)
+    elif st.op == "gather":
+        kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, d["spt"], d["reqs"], err)
+    else:
+        kvx.kvx_scatter(mem[st.src], S, mem[st.dst], D, d["dpt"], d["reqs"], err)
+    torch.cuda.synchronize()
+    return int(err.item())
+
+
+def _free(torch, *objs):
+    del objs
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("k", [2, 3, 4])
+def test_full_transfer(torch, k):
+    from oracle import layer_check
+    wl, mem, dsteps = _setup(torch, k)
+    st = dsteps[0]["st"]
+    src = mem[st.src]
+    before = int(src.view(torch.int64).sum().item())
+    print(f"config {k}: {wl.title}", flush=True)
+    for _ in range(2):                       # repeated launches write the same bytes
+        assert _run(torch, wl, mem, dsteps[0]) == 0
+    assert int(src.view(torch.int64).sum().item()) == before, "source pool modified"
+    S, D = wl.sides[st.src], wl.sides[st.dst]
+    for l in sorted({0, S.L // 2, S.L - 1}):
+        r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l, wl.prefill_tag)
+        print(f"  layer {l}: oracle {r.oracle_seconds:.2f} s, equal={r.equal}", flush=True)
+        assert r.equal, f"config {k} layer {l} differs from the oracle"
+    _free(torch, mem, dsteps)
+
+
+def test_full_host_offload_onload(torch):
+    from oracle import layer_check
+    wl, mem, dsteps = _setup(torch, 5)
+    g, s = wl.steps
+    S, B = wl.sides["A"], wl.sides["buf"]
+    layers = sorted({0, S.L // 2, S.L - 1})
+    before = {l: layer_check.pool_layer(mem["A"], S, l) for l in layers}
+    assert _run(torch, wl, mem, dsteps[0]) == 0       # offload to pinned host memory
+    assert _run(torch, wl, mem, dsteps[1]) == 0       # onload into fresh pages
+    for l in layers:
+        after = layer_check.pool_layer(mem["A"], S, l)
+        ok_g, ok_s = layer_check.gather_scatter_layer(before[l], S, mem["buf"], B, after, g, s, l)
+        print(f"  layer {l}: offload equal={ok_g}, onload equal={ok_s}", flush=True)
+        assert ok_g and ok_s
+        # round trip: new page k holds the pre-offload bytes of original page k
+        per_page = S.nbytes // S.L // S.N
+        old = before[l].reshape(S.N, per_page)[g.src_pt]
+        new = after.reshape(S.N, per_page)[s.dst_pt]
+        assert np.array_equal(old, new)
+    _free(torch, mem, dsteps)

@@ -1,0 +1,92 @@
+"""The seeded input recipe: shapes, sizes and page-table structure of the five
+workloads, and determinism of every generator."""
+import numpy as np
+import pytest
+
+from paper_2606_31093_amd import workloads as W
+
+
+def _pages_needed(start, n, T):
+    return -(-(start + n) // T) if n else 0
+
+
+@pytest.mark.parametrize("k,small", [(1, False), (2, False), (3, False), (4, False), (5, False),
+                                     (2, True), (3, True), (4, True), (5, True)])
+def test_tables_cover_and_destinations_are_disjoint(k, small):
+    wl = W.config(k, small=small)
+    for st in wl.steps:
+        used_dst = set()
+        for so, do, bo, s0, d0, n in st.reqs:
+            if st.src_pt is not None:
+                k_s = _pages_needed(s0, n, wl.sides[st.src].T)
+                pages = st.src_pt[so: so + k_s]
+                assert len(pages) == k_s and ((pages >= 0) & (pages < wl.sides[st.src].N)).all()
+            if st.dst_pt is not None:
+                Dp = wl.sides[st.dst]
+                k_d = _pages_needed(d0, n, Dp.T)
+                pages = st.dst_pt[do: do + k_d]
+                assert len(pages) == k_d and ((pages >= 0) & (pages < Dp.N)).all()
+                # destination slots written by different requests never overlap
+                first, last = d0 // Dp.T, (d0 + n - 1) // Dp.T
+                for j, p in enumerate(pages[first:last + 1]):
+                    assert (p, first + j) not in used_dst
+                    used_dst.add((int(p), first + j))
+            else:
+                B = wl.sides[st.dst]
+                assert bo >= 0 and bo + B.L * B.C * n * B.H * B.D <= B.cap
+        assert len(np.unique(st.dst_pt)) == len(st.dst_pt) if st.dst_pt is not None else True
+
+
+def test_deterministic():
+    for k in (1, 2, 3, 4, 5):
+        a, b = W.config(k), W.config(k)
+        for sa, sb in zip(a.steps, b.steps):
+            assert np.array_equal(sa.reqs, sb.reqs)
+            for x, y in ((sa.src_pt, sb.src_pt), (sa.dst_pt, sb.dst_pt)):
+                assert (x is None and y is None) or np.array_equal(x, y)
+    assert np.array_equal(W.normal_bf16_bytes(64, 3), W.normal_bf16_bytes(64, 3))
+    assert np.array_equal(W.prefill_bytes(64, 9, 8), W.prefill_bytes(72, 9)[8:])
+
+
+def test_stated_shapes():
+    c2 = W.config(2)
+    A = c2.sides["A"]
+    assert (A.L, A.C, A.H, A.D, A.T, A.N, A.layout) == (36, 2, 8, 128, 64, 4096, "LPCTHD")
+    assert A.nbytes == 36 * 2**30 and len(c2.steps[0].reqs) == 32
+    n = c2.steps[0].reqs[:, 5]
+    assert n.min() >= 1024 and n.max() <= 8192
+    c3 = W.config(3)
+    assert (c3.sides["A"].T, c3.sides["A"].layout, c3.sides["B"].T, c3.sides["B"].layout) == \
+        (16, "LPCTHD", 64, "PLCHTD")
+    lens = np.array(c3.notes["lengths"])
+    assert len(lens) == 16 and lens.min() >= 2048 and lens.max() <= 16384
+    c4 = W.config(4)
+    A4 = c4.sides["A"]
+    assert (A4.L, A4.C, A4.H, A4.D, A4.T) == (61, 1, 1, 576, 64)
+    lens, starts = np.array(c4.notes["lengths"]), np.array(c4.notes["starts"])
+    assert len(lens) == 64 and lens.min() >= 4096 and lens.max() <= 32768
+    assert (starts >= 0).all() and (starts < lens // 2).all()
+    assert (starts % 64 != 0).any()          # unaligned partial prefixes occur
+    r = c4.steps[0].reqs
+    assert (r[:, 3] == starts).all() and (r[:, 4] == starts).all() and (r[:, 5] == lens - starts).all()
+    c5 = W.config(5)
+    g, s = c5.steps
+    assert len(g.src_pt) == 1820 and len(np.unique(g.src_pt)) == 1820
+    assert len(np.unique(s.dst_pt)) == 1820
+    assert c5.sides["buf"].nbytes == 1820 * 9 * 2**20     # 16 GiB subset: 1820 pages x 9 MiB
+    assert c5.host_sides == ("buf",)
+    c1 = W.config(1)
+    assert len(c1.steps[0].src_pt) == 7 and len(c1.steps[1].dst_pt) == 4
+
+
+def test_prefill_is_offset_coded():
+    b = W.prefill_bytes(64, 0x33).view("<u8")
+    assert [int(x) & 0xFFFFFFFFFFFF for x in b] == list(range(8))
+    assert all((int(x) >> 48) == 0x5A33 for x in b)
+
+
+def test_bf16_rounding_nearest_even():
+    x = W.normal_bf16_bytes(1 << 12, 5).view("<u2")
+    # values decode to roughly N(0, 1)
+    f = (x.astype(np.uint32) << 16).view(np.float32)
+    assert abs(float(f.mean())) < 0.1 and 0.9 < float(f.std()) < 1.1
