@@ -7,8 +7,9 @@ role handoff:
 - 36 layers x 8 KV heads x 128 head_dim, bf16;
 - 4096 x 64-token pools on both sides, layout [layer][page][kv][token][head][dim];
 - 32 requests with lengths uniform in [1024, 8192] on random page tables.
-A step is one fused kvx_transfer of all 32 requests.  ``--config 3/4/5``
-selects the relayout, MLA partial-prefix and host-tier workloads.
+A step is one fused kvx_transfer of all 32 requests.  ``--workload
+relayout|mla|host_tier`` selects the relayout, MLA partial-prefix and
+host-tier workloads.
 
 GB/s counts algorithmic bytes, GB = 1e9: every copied token position is read
 once and written once, 2 * tokens * L*C*H*D*e per step.
@@ -57,7 +58,7 @@ def kernel_sha() -> str:
 def traffic_record(key: int):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
     if it was taken on the current kernel sources."""
-    path = os.path.join(ROOT, "profiles", f"traffic_config{key}.json")
+    path = os.path.join(ROOT, "profiles", f"traffic_{key}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -72,7 +73,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, choices=[2, 3, 4, 5])
+    ap.add_argument("--workload", default="handoff",
+                    choices=["handoff", "relayout", "mla", "host_tier"])
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="layers of the workload the CPU oracle runs (0: skip)")
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
@@ -119,7 +121,7 @@ def main() -> int:
     kvx.lib()
 
     dev = torch.device("cuda", 0)
-    wl = workloads.config(args.config)
+    wl = workloads.get(args.workload)
     log(f"workload: {wl.title}")
     mem = {}
     for name, spec in wl.sides.items():
@@ -187,7 +189,7 @@ def main() -> int:
     dom_bytes = wl.algorithmic_bytes(dom)
     achieved = dom_bytes / (kern_ms[i_dom] / 1e3) / 1e9
     host_leg = bool(wl.host_sides)
-    tr = traffic_record(args.config)
+    tr = traffic_record(args.workload)
     if host_leg:
         one_way = dom_bytes / 2
         roofline = {"bound": "pcie", "achieved": round(one_way / (kern_ms[i_dom] / 1e3) / 1e9, 2),
@@ -275,7 +277,7 @@ def main() -> int:
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u16",
         "data": "synthetic (seeded N(0,1) bf16 source, offset-coded destination prefill)",
-        "config": {"workload": wl.title, "config": args.config,
+        "config": {"workload": wl.title, "name": args.workload,
                    "ops": [st.op for st in wl.steps], "requests": len(wl.steps[0].reqs),
                    "tokens_per_step": n_tok, "bytes_per_step": step_bytes,
                    "pools": {k: {"bytes": v.nbytes, **({"layout": v.layout, "page_tokens": v.T}

@@ -48,9 +48,11 @@ class _Buf(ctypes.Structure):
 
 def build(source: str = SOURCE, output: str = LIBRARY) -> str:
     """Compile the oracle with gcc (plain -O2, no vector intrinsics)."""
+    tmp = f"{output}.tmp{os.getpid()}"
     cmd = ["gcc", "-O2", "-std=c99", "-Wall", "-Werror", "-shared", "-fPIC",
-           "-o", output, source]
+           "-o", tmp, source]
     subprocess.run(cmd, check=True)
+    os.replace(tmp, output)        # atomic: concurrent test workers may build too
     return output
 
 

@@ -36,7 +36,7 @@ def command(output: str = LIBRARY, defines=()) -> list:
 
 
 def build(output: str = LIBRARY, defines=(), quiet: bool = True) -> str:
-    tmp = output + ".tmp"
+    tmp = f"{output}.tmp{os.getpid()}"
     r = subprocess.run(command(tmp, defines), capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed:\n{r.stdout}\n{r.stderr}")

@@ -15,7 +15,7 @@ L2 CPU tier migration, Sec. 4.1.2):
   2. LLM role handoff (36 layers x 8 KV heads x 128, 64-token pages, 32 requests)
   3. heterogeneous relayout (28 x 4 x 128, 16-token LPCTHD -> 64-token PLCHTD)
   4. MLA latent cache (61 layers x 576, 64-token pages, copy of [p, len))
-  5. host-tier offload then onload of a 16 GiB page subset (config-2 shape)
+  5. host-tier offload then onload of a 16 GiB page subset (handoff shape)
 
 Each has a ``small`` variant with the same layouts, page sizes and row widths
 but fewer layers, heads, pages and tokens, for parity checks the oracle
@@ -98,7 +98,7 @@ class Step:
 
 @dataclass
 class Workload:
-    key: int
+    name: str
     title: str
     sides: dict                  # name -> PoolSpec | BufSpec
     steps: list
@@ -137,7 +137,7 @@ def _take_pages(perm: np.ndarray, counts) -> tuple[np.ndarray, list]:
 # the five workloads
 # --------------------------------------------------------------------------
 
-def config1() -> Workload:
+def tiny() -> Workload:
     """2 layers, 2 KV heads, head_dim 64; a 100-token request on 7 random
     pages of a 64 x 16-token pool is gathered to a flat buffer, which is then
     scattered into a 32 x 32-token pool on 4 random pages."""
@@ -151,12 +151,12 @@ def config1() -> Workload:
     dst_pt = rng.permutation(dst.N)[: _ceil_div(n, dst.T)].astype(np.int32)
     gather = Step("gather", "A", "buf", src_pt, None, _reqs([0, 0, 0, 0, 0, n]))
     scatter = Step("scatter", "buf", "B", None, dst_pt, _reqs([0, 0, 0, 0, 0, n]))
-    return Workload(1, "tiny gather->flat->scatter, 2L x 2H x 64, 16->32-token pages",
+    return Workload("tiny", "tiny gather->flat->scatter, 2L x 2H x 64, 16->32-token pages",
                     {"A": src, "buf": buf, "B": dst}, [gather, scatter],
                     value_seed=2001, prefill_tag=1)
 
 
-def _transfer_workload(key, title, src: PoolSpec, dst: PoolSpec, lengths, starts,
+def _transfer_workload(name, seed_key, title, src: PoolSpec, dst: PoolSpec, lengths, starts,
                        rng, notes=None) -> Workload:
     """Requests hold positions [0, len); the copy moves [start, len) to the
     same positions.  Each side draws one permutation of its pages and gives
@@ -169,14 +169,14 @@ def _transfer_workload(key, title, src: PoolSpec, dst: PoolSpec, lengths, starts
     dst_pt, dst_off = _take_pages(dst_perm, [_ceil_div(n, dst.T) for n in lengths])
     rows = [[so, do, 0, p, p, n - p] for so, do, p, n in zip(src_off, dst_off, starts, lengths)]
     step = Step("transfer", "A", "B", src_pt, dst_pt, _reqs(rows))
-    wl = Workload(key, title, {"A": src, "B": dst}, [step],
-                  value_seed=2000 + key, prefill_tag=key, notes=notes or {})
+    wl = Workload(name, title, {"A": src, "B": dst}, [step],
+                  value_seed=2000 + seed_key, prefill_tag=seed_key, notes=notes or {})
     wl.notes.setdefault("lengths", lengths)
     wl.notes.setdefault("starts", starts)
     return wl
 
 
-def config2(small: bool = False) -> Workload:
+def handoff(small: bool = False) -> Workload:
     """LLM role handoff: 36 layers, 8 KV heads, head_dim 128, 4096 x 64-token
     pools on both sides, 32 requests with lengths uniform in [1024, 8192]."""
     if small:
@@ -187,11 +187,11 @@ def config2(small: bool = False) -> Workload:
         L, H, N, nreq, lo, hi = 36, 8, 4096, 32, 1024, 8192
     pool = PoolSpec(L, 2, H, 128, T=64, N=N, e=2, layout="LPCTHD")
     lengths = rng.integers(lo, hi + 1, size=nreq)
-    return _transfer_workload(2, f"LLM role handoff {L}L x {H}H x 128, 64-token pages, "
+    return _transfer_workload("handoff", 2, f"LLM role handoff {L}L x {H}H x 128, 64-token pages, "
                               f"{nreq} requests", pool, pool, lengths, [0] * nreq, rng)
 
 
-def config3(small: bool = False) -> Workload:
+def relayout(small: bool = False) -> Workload:
     """Heterogeneous-role relayout: 28 layers, 4 KV heads, head_dim 128;
     16-token LPCTHD pages into 64-token PLCHTD pages; 16 requests with
     lengths uniform in [2048, 16384]."""
@@ -204,11 +204,11 @@ def config3(small: bool = False) -> Workload:
     src = PoolSpec(L, 2, 4, 128, T=16, N=Ns, e=2, layout="LPCTHD")
     dst = PoolSpec(L, 2, 4, 128, T=64, N=Nd, e=2, layout="PLCHTD")
     lengths = rng.integers(lo, hi + 1, size=nreq)
-    return _transfer_workload(3, f"relayout {L}L x 4H x 128, 16-token LPCTHD -> 64-token "
+    return _transfer_workload("relayout", 3, f"relayout {L}L x 4H x 128, 16-token LPCTHD -> 64-token "
                               f"PLCHTD, {nreq} requests", src, dst, lengths, [0] * nreq, rng)
 
 
-def config4(small: bool = False) -> Workload:
+def mla(small: bool = False) -> Workload:
     """MLA-style compressed KV: 61 layers, one 576-wide latent (C = 1, H = 1),
     64-token pages; 64 requests with lengths uniform in [4096, 32768]; only
     positions [p, len) are copied, p uniform in [0, len/2)."""
@@ -223,12 +223,12 @@ def config4(small: bool = False) -> Workload:
     pages = sum(_ceil_div(int(n), 64) for n in lengths)
     N = _ceil_div(pages, align) * align
     pool = PoolSpec(L, 1, 1, 576, T=64, N=N, e=2, layout="LPCTHD")
-    return _transfer_workload(4, f"MLA latent {L}L x 576, 64-token pages, {nreq} requests, "
+    return _transfer_workload("mla", 4, f"MLA latent {L}L x 576, 64-token pages, {nreq} requests, "
                               f"partial prefix [p, len)", pool, pool, lengths, starts, rng)
 
 
-def config5(small: bool = False) -> Workload:
-    """Host-tier offload/onload: the config-2 pool; a 16 GiB subset of random
+def host_tier(small: bool = False) -> Workload:
+    """Host-tier offload/onload: the handoff pool; a 16 GiB subset of random
     pages (1820 pages = 28 requests x 65 full pages) is gathered into a
     pinned host buffer [request][layer][kv][token][head][dim] and scattered
     back into a fresh random sample of pool pages."""
@@ -248,15 +248,20 @@ def config5(small: bool = False) -> Workload:
     s_rows = [[0, r * per, r * block, 0, 0, n] for r in range(nreq)]
     steps = [Step("gather", "A", "buf", out_pages, None, _reqs(g_rows)),
              Step("scatter", "buf", "A", None, in_pages, _reqs(s_rows))]
-    return Workload(5, f"host-tier offload/onload {L}L x {H}H x 128, {nreq * per} pages "
+    return Workload("host_tier", f"host-tier offload/onload {L}L x {H}H x 128, {nreq * per} pages "
                     f"({nreq} x {per})", {"A": pool, "buf": buf}, steps,
                     value_seed=2005, prefill_tag=5, host_sides=("buf",))
 
 
-def config(k: int, small: bool = False) -> Workload:
-    if k == 1:
-        return config1()
-    return {2: config2, 3: config3, 4: config4, 5: config5}[k](small=small)
+NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier")
+
+
+def get(name: str, small: bool = False) -> Workload:
+    """A workload by name; ``small`` shrinks every one but ``tiny``."""
+    if name == "tiny":
+        return tiny()
+    return {"handoff": handoff, "relayout": relayout, "mla": mla,
+            "host_tier": host_tier}[name](small=small)
 
 
 def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:

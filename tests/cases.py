@@ -46,7 +46,7 @@ def transfer_case(ls, ld, Ts, Td, seed, *, e=2, D=8, L=2, C=2, H=3, spec=None,
         dst_pt.extend(dperm[len(dst_pt): len(dst_pt) + k_d])
     step = Step("transfer", "A", "B", np.asarray(src_pt, np.int32), np.asarray(dst_pt, np.int32),
                 np.asarray(rows, np.int64).reshape(-1, 6))
-    return Workload(0, f"transfer {ls}/T{Ts} -> {ld}/T{Td} e{e} D{D} L{L} C{C} H{H}",
+    return Workload("case", f"transfer {ls}/T{Ts} -> {ld}/T{Td} e{e} D{D} L{L} C{C} H{H}",
                     {"A": S, "B": Dp}, [step], value_seed=seed, prefill_tag=seed & 0xFF)
 
 
@@ -74,7 +74,7 @@ def gather_scatter_case(layout, T, e, D, seed, *, L=3, C=2, H=2, pinned=False) -
     dperm = rng.permutation(S.N).astype(np.int32)[: len(pt)]
     steps = [Step("gather", "A", "buf", np.asarray(pt, np.int32), None, np.asarray(g_rows, np.int64)),
              Step("scatter", "buf", "B", None, dperm, np.asarray(s_rows, np.int64))]
-    return Workload(0, f"gather/scatter {layout} T{T} e{e} D{D}", {"A": S, "buf": B, "B": S},
+    return Workload("case", f"gather/scatter {layout} T{T} e{e} D{D}", {"A": S, "buf": B, "B": S},
                     steps, value_seed=seed, prefill_tag=seed & 0xFF,
                     host_sides=("buf",) if pinned else ())
 

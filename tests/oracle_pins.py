@@ -35,7 +35,7 @@ for p in (ROOT, HERE):
 
 import np_reference as npr  # noqa: E402
 from paper_2606_31093_amd.workloads import (  # noqa: E402
-    LAYOUTS, BufSpec, PoolSpec, config1, normal_bf16_bytes, prefill_bytes, random_bytes)
+    LAYOUTS, BufSpec, PoolSpec, tiny, normal_bf16_bytes, prefill_bytes, random_bytes)
 
 ERR_SRC_PAGE, ERR_DST_PAGE, ERR_PT_RANGE, ERR_BAD_REQ = 1, 2, 4, 8
 
@@ -435,8 +435,8 @@ def pin_max_position(O):
 # the tiny workload end to end
 # ---------------------------------------------------------------------------
 
-def pin_config1(O):
-    wl = config1()
+def pin_tiny_workload(O):
+    wl = tiny()
     A, buf, B = wl.sides["A"], wl.sides["buf"], wl.sides["B"]
     g, s = wl.steps
     a = normal_bf16_bytes(A.nbytes, wl.value_seed)
@@ -444,21 +444,21 @@ def pin_config1(O):
     npr.gather(a, A, want_buf, buf, g.src_pt, g.reqs)
     got_buf = np.zeros(buf.nbytes, np.uint8)
     assert O.gather(a, A, got_buf, buf, g.src_pt, g.reqs) == 0
-    _same(got_buf, want_buf, "config 1 gather")
+    _same(got_buf, want_buf, "tiny gather")
     b0 = prefill_bytes(B.nbytes, wl.prefill_tag)
     want_b, got_b = b0.copy(), b0.copy()
     npr.scatter(want_buf, buf, want_b, B, s.dst_pt, s.reqs)
     assert O.scatter(got_buf, buf, got_b, B, s.dst_pt, s.reqs) == 0
-    _same(got_b, want_b, "config 1 scatter")
+    _same(got_b, want_b, "tiny scatter")
     back = np.zeros(buf.nbytes, np.uint8)
     assert O.gather(got_b, B, back, buf, s.dst_pt,
                     [[0, 0, 0, 0, 0, int(s.reqs[0, 5])]]) == 0
-    _same(back, got_buf, "config 1 round trip")
+    _same(back, got_buf, "tiny round trip")
 
 
 PINS = [pin_hand_example, pin_hand_example_plchtd, pin_numpy_transfer,
         pin_numpy_transfer_widths, pin_numpy_gather_scatter, pin_identity_tables,
-        pin_roundtrip, pin_bijection, pin_errors, pin_max_position, pin_config1]
+        pin_roundtrip, pin_bijection, pin_errors, pin_max_position, pin_tiny_workload]
 
 
 def run_all(O) -> list:

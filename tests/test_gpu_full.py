@@ -19,7 +19,7 @@ def torch():
 
 def _setup(torch, k):
     from paper_2606_31093_amd import kvx, workloads
-    wl = workloads.config(k)
+    wl = workloads.get(k)
     dev = torch.device("cuda", 0)
     mem = {n: workloads.alloc_side(s, dev, pinned=n in wl.host_sides) for n, s in wl.sides.items()}
     workloads.init_sides_(wl, mem)
@@ -51,14 +51,14 @@ def _free(torch, *objs):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("k", [2, 3, 4])
+@pytest.mark.parametrize("k", ["handoff", "relayout", "mla"])
 def test_full_transfer(torch, k):
     from oracle import layer_check
     wl, mem, dsteps = _setup(torch, k)
     st = dsteps[0]["st"]
     src = mem[st.src]
     before = int(src.view(torch.int64).sum().item())
-    print(f"config {k}: {wl.title}", flush=True)
+    print(f"{k}: {wl.title}", flush=True)
     for _ in range(2):                       # repeated launches write the same bytes
         assert _run(torch, wl, mem, dsteps[0]) == 0
     assert int(src.view(torch.int64).sum().item()) == before, "source pool modified"
@@ -66,13 +66,13 @@ def test_full_transfer(torch, k):
     for l in sorted({0, S.L // 2, S.L - 1}):
         r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l, wl.prefill_tag)
         print(f"  layer {l}: oracle {r.oracle_seconds:.2f} s, equal={r.equal}", flush=True)
-        assert r.equal, f"config {k} layer {l} differs from the oracle"
+        assert r.equal, f"{k} layer {l} differs from the oracle"
     _free(torch, mem, dsteps)
 
 
 def test_full_host_offload_onload(torch):
     from oracle import layer_check
-    wl, mem, dsteps = _setup(torch, 5)
+    wl, mem, dsteps = _setup(torch, "host_tier")
     g, s = wl.steps
     S, B = wl.sides["A"], wl.sides["buf"]
     layers = sorted({0, S.L // 2, S.L - 1})

@@ -7,7 +7,7 @@ import numpy as np
 import pytest
 
 import cases
-from paper_2606_31093_amd.workloads import PoolSpec, BufSpec, Step, Workload, config
+from paper_2606_31093_amd.workloads import PoolSpec, BufSpec, Step, Workload, get
 from runner import assert_same, initial_bytes, run_gpu, run_oracle
 
 pytestmark = pytest.mark.gpu
@@ -31,13 +31,13 @@ def check(wl, raw_reqs=None, oracle_reqs=None):
     return got, gerr
 
 
-def test_config1_tiny():
-    check(config(1))
+def test_tiny_workload():
+    check(get("tiny"))
 
 
-@pytest.mark.parametrize("k", [2, 3, 4, 5])
-def test_small_configs(k):
-    check(config(k, small=True))
+@pytest.mark.parametrize("name", ["handoff", "relayout", "mla", "host_tier"])
+def test_small_workloads(name):
+    check(get(name, small=True))
 
 
 @pytest.mark.parametrize("ls,ld,Ts,Td", list(cases.layout_matrix()),
@@ -83,7 +83,7 @@ def test_many_requests_and_empty_ones():
 
 def _err_wl(src_pt, dst_pt, rows, N=4, T=4):
     S = PoolSpec(1, 2, 1, 8, T=T, N=N, e=2, layout="LPCTHD")
-    return Workload(0, f"errors {rows}", {"A": S, "B": S},
+    return Workload("case", f"errors {rows}", {"A": S, "B": S},
                     [Step("transfer", "A", "B", np.asarray(src_pt, np.int32),
                           np.asarray(dst_pt, np.int32), np.asarray(rows, np.int64).reshape(-1, 6))],
                     value_seed=3, prefill_tag=9)
@@ -114,13 +114,13 @@ def test_buffer_record_errors():
     B = BufSpec(1, 2, 1, 8, 2, cap=2 * n * 8 + 8)
     for row, bits in (([0, 0, 8, 0, 0, n], 0), ([0, 0, 0, 0, 0, n], 0), ([0, 0, 16, 0, 0, n], 8),
                       ([0, 0, 4, 0, 0, n], 8), ([0, 0, -8, 0, 0, n], 8), ([0, 0, 0, 0, 1, n], 8)):
-        wl = Workload(0, f"gather {row}", {"A": S, "buf": B},
+        wl = Workload("case", f"gather {row}", {"A": S, "buf": B},
                       [Step("gather", "A", "buf", np.asarray([0, 1], np.int32), None,
                             np.asarray([row], np.int64))], value_seed=1, prefill_tag=2)
         _, errs = check(wl)
         assert errs == [bits]
     for row, bits in (([0, 0, 8, 0, 0, n], 0), ([0, 0, 16, 0, 0, n], 8), ([0, 0, 0, 2, 0, n], 8)):
-        wl = Workload(0, f"scatter {row}", {"buf": B, "B": S},
+        wl = Workload("case", f"scatter {row}", {"buf": B, "B": S},
                       [Step("scatter", "buf", "B", None, np.asarray([2, 3], np.int32),
                             np.asarray([row], np.int64))], value_seed=1, prefill_tag=2)
         _, errs = check(wl)
@@ -145,7 +145,7 @@ def test_max_position():
     T = 1 << 16
     S = PoolSpec(1, 1, 1, 8, T=T, N=1, e=2, layout="LPCTHD")
     B = BufSpec(1, 1, 1, 8, 2, cap=5 * 8)
-    wl = Workload(0, "max position", {"A": S, "buf": B},
+    wl = Workload("case", "max position", {"A": S, "buf": B},
                   [Step("gather", "A", "buf", np.zeros(32768, np.int32), None,
                         np.asarray([[0, 0, 0, 2**31 - 6, 0, 5]], np.int64))],
                   value_seed=4, prefill_tag=4)
@@ -169,7 +169,7 @@ def test_side_stream():
     """Work runs on the stream passed in, ordered with other work there."""
     import torch
     from paper_2606_31093_amd import kvx
-    wl = config(2, small=True)
+    wl = get("handoff", small=True)
     init = initial_bytes(wl)
     want, _ = run_oracle(wl, init)
     st = wl.steps[0]

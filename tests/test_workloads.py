@@ -10,10 +10,11 @@ def _pages_needed(start, n, T):
     return -(-(start + n) // T) if n else 0
 
 
-@pytest.mark.parametrize("k,small", [(1, False), (2, False), (3, False), (4, False), (5, False),
-                                     (2, True), (3, True), (4, True), (5, True)])
+@pytest.mark.parametrize("k,small", [("tiny", False), ("handoff", False), ("relayout", False),
+                                     ("mla", False), ("host_tier", False), ("handoff", True),
+                                     ("relayout", True), ("mla", True), ("host_tier", True)])
 def test_tables_cover_and_destinations_are_disjoint(k, small):
-    wl = W.config(k, small=small)
+    wl = W.get(k, small=small)
     for st in wl.steps:
         used_dst = set()
         for so, do, bo, s0, d0, n in st.reqs:
@@ -38,8 +39,8 @@ def test_tables_cover_and_destinations_are_disjoint(k, small):
 
 
 def test_deterministic():
-    for k in (1, 2, 3, 4, 5):
-        a, b = W.config(k), W.config(k)
+    for k in W.NAMES:
+        a, b = W.get(k), W.get(k)
         for sa, sb in zip(a.steps, b.steps):
             assert np.array_equal(sa.reqs, sb.reqs)
             for x, y in ((sa.src_pt, sb.src_pt), (sa.dst_pt, sb.dst_pt)):
@@ -49,18 +50,18 @@ def test_deterministic():
 
 
 def test_stated_shapes():
-    c2 = W.config(2)
+    c2 = W.get("handoff")
     A = c2.sides["A"]
     assert (A.L, A.C, A.H, A.D, A.T, A.N, A.layout) == (36, 2, 8, 128, 64, 4096, "LPCTHD")
     assert A.nbytes == 36 * 2**30 and len(c2.steps[0].reqs) == 32
     n = c2.steps[0].reqs[:, 5]
     assert n.min() >= 1024 and n.max() <= 8192
-    c3 = W.config(3)
+    c3 = W.get("relayout")
     assert (c3.sides["A"].T, c3.sides["A"].layout, c3.sides["B"].T, c3.sides["B"].layout) == \
         (16, "LPCTHD", 64, "PLCHTD")
     lens = np.array(c3.notes["lengths"])
     assert len(lens) == 16 and lens.min() >= 2048 and lens.max() <= 16384
-    c4 = W.config(4)
+    c4 = W.get("mla")
     A4 = c4.sides["A"]
     assert (A4.L, A4.C, A4.H, A4.D, A4.T) == (61, 1, 1, 576, 64)
     lens, starts = np.array(c4.notes["lengths"]), np.array(c4.notes["starts"])
@@ -69,13 +70,13 @@ def test_stated_shapes():
     assert (starts % 64 != 0).any()          # unaligned partial prefixes occur
     r = c4.steps[0].reqs
     assert (r[:, 3] == starts).all() and (r[:, 4] == starts).all() and (r[:, 5] == lens - starts).all()
-    c5 = W.config(5)
+    c5 = W.get("host_tier")
     g, s = c5.steps
     assert len(g.src_pt) == 1820 and len(np.unique(g.src_pt)) == 1820
     assert len(np.unique(s.dst_pt)) == 1820
     assert c5.sides["buf"].nbytes == 1820 * 9 * 2**20     # 16 GiB subset: 1820 pages x 9 MiB
     assert c5.host_sides == ("buf",)
-    c1 = W.config(1)
+    c1 = W.get("tiny")
     assert len(c1.steps[0].src_pt) == 7 and len(c1.steps[1].dst_pt) == 4
 
 
