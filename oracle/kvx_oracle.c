@@ -243,3 +243,56 @@ uint32_t ora_scatter(const uint8_t *src, const ora_buf *B, uint8_t *dst,
     }
     return err;
 }
+
+/* Slice of a pool -> slice of another pool (Sec. 4.1.1: a view names a
+ * tuple of layers and a tuple of slices; Sec. 4.1.3: one node may hold the
+ * K half of a page and another the V half; Sec. 7: transfers between
+ * different tensor-parallel layouts).
+ *
+ * sl[] = { src_layer0, dst_layer0, n_layers, src_kv0, dst_kv0, n_kv,
+ *          src_head0, dst_head0, n_heads }
+ * For every request r, i in [0, n_r), l < n_layers, c < n_kv, h < n_heads,
+ * d < head_dim:
+ *   DST(dst_layer0 + l, dst_kv0 + c, pd, dst_head0 + h, d)
+ *       := SRC(src_layer0 + l, src_kv0 + c, ps, src_head0 + h, d)
+ * The pools may differ in layers, kv components and heads; head_dim and
+ * element size match.  Same resolution and error rules as ora_transfer. */
+uint32_t ora_transfer_slice(const uint8_t *src, const ora_pool *S, uint8_t *dst,
+                            const ora_pool *Dp, const int64_t *sl,
+                            const int32_t *src_pt, int64_t src_pt_len,
+                            const int32_t *dst_pt, int64_t dst_pt_len,
+                            const int64_t *reqs, int64_t n_reqs)
+{
+    uint32_t err = 0;
+    for (int64_t r = 0; r < n_reqs; ++r) {
+        const int64_t *q = reqs + 6 * r;
+        int64_t n = q[R_N];
+        if (!range_ok(q[R_SRC_START], n) || !range_ok(q[R_DST_START], n)) {
+            err |= ORA_ERR_BAD_REQ;
+            continue;
+        }
+        for (int64_t i = 0; i < n; ++i) {
+            int64_t ps = q[R_SRC_START] + i, pd = q[R_DST_START] + i;
+            int64_t sp, ss, dp, ds;
+            int bad = resolve(Dp, dst_pt, dst_pt_len, q[R_DST_PT], pd,
+                              ORA_ERR_DST_PAGE, &dp, &ds);
+            if (!bad)
+                bad = resolve(S, src_pt, src_pt_len, q[R_SRC_PT], ps,
+                              ORA_ERR_SRC_PAGE, &sp, &ss);
+            if (bad) {
+                err |= (uint32_t)bad;
+                continue;
+            }
+            for (int64_t l = 0; l < sl[2]; ++l)
+                for (int64_t c = 0; c < sl[5]; ++c)
+                    for (int64_t h = 0; h < sl[8]; ++h)
+                        for (int64_t d = 0; d < S->D; ++d)
+                            copy_elem(dst + Dp->e * pool_index(Dp, sl[1] + l, sl[4] + c, dp, ds,
+                                                               sl[7] + h, d),
+                                      src + S->e * pool_index(S, sl[0] + l, sl[3] + c, sp, ss,
+                                                              sl[6] + h, d),
+                                      S->e);
+        }
+    }
+    return err;
+}

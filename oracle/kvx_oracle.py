@@ -116,6 +116,8 @@ class Oracle:
         lib.ora_gather.restype = u32
         lib.ora_scatter.argtypes = [vp, bp, vp, pp, vp, i64, vp, i64]
         lib.ora_scatter.restype = u32
+        lib.ora_transfer_slice.argtypes = [vp, pp, vp, pp, vp, vp, i64, vp, i64, vp, i64]
+        lib.ora_transfer_slice.restype = u32
         self.lib = lib
 
     def transfer(self, src: np.ndarray, src_shape, dst: np.ndarray, dst_shape,
@@ -159,6 +161,33 @@ class Oracle:
             _ptr(dp), np.asarray(dst_pt).size, _ptr(rq), nr))
 
 
+    def transfer_slice(self, src: np.ndarray, src_shape, dst: np.ndarray, dst_shape, sl,
+                       src_pt, dst_pt, reqs) -> int:
+        """Slice of a pool -> slice of another pool.  ``sl`` is (src_layer0,
+        dst_layer0, n_layers, src_kv0, dst_kv0, n_kv, src_head0, dst_head0,
+        n_heads); each range must lie inside both pools."""
+        sl = [int(x) for x in sl]
+        if len(sl) != 9:
+            raise ValueError("a slice has nine fields")
+        for (o_s, o_d, cnt), ks in ((sl[0:3], "L"), (sl[3:6], "C"), (sl[6:9], "H")):
+            if cnt < 0 or o_s < 0 or o_d < 0 or o_s + cnt > getattr(src_shape, ks) \
+                    or o_d + cnt > getattr(dst_shape, ks):
+                raise ValueError(f"slice range {ks} does not fit the pools")
+        for k in ("D", "e"):
+            if getattr(src_shape, k) != getattr(dst_shape, k):
+                raise ValueError(f"element shapes differ in {k}")
+        _bytes(src, pool_elems(src_shape) * src_shape.e, "src")
+        _bytes(dst, pool_elems(dst_shape) * dst_shape.e, "dst", writable=True)
+        sp, dp = _i32(src_pt), _i32(dst_pt)
+        rq, nr = _reqs(reqs)
+        S, D = _pool(src_shape), _pool(dst_shape)
+        slc = np.asarray(sl, dtype=np.int64)
+        return int(self.lib.ora_transfer_slice(
+            _ptr(src), ctypes.byref(S), _ptr(dst), ctypes.byref(D), _ptr(slc),
+            _ptr(sp), np.asarray(src_pt).size, _ptr(dp), np.asarray(dst_pt).size,
+            _ptr(rq), nr))
+
+
 _DEFAULT: Oracle | None = None
 
 
@@ -182,3 +211,7 @@ def gather(*a, **k) -> int:
 
 def scatter(*a, **k) -> int:
     return default().scatter(*a, **k)
+
+
+def transfer_slice(*a, **k) -> int:
+    return default().transfer_slice(*a, **k)

@@ -70,3 +70,17 @@ def scatter(src, B, dst, Dp, dst_pt, reqs) -> None:
             continue
         dp, ds = _where(np.asarray(dst_pt), do, d0, n, Dp.T)
         Vd[:, dp, :, ds, :, :] = np.moveaxis(block(src, B, bo, n), 2, 0)
+
+
+def transfer_slice(src, S, dst, Dp, sl, src_pt, dst_pt, reqs) -> None:
+    """Slice copy: layers, kv components and heads are numpy slices of the
+    6-D views, each offset on its own side."""
+    sl0, dl0, nl, sc0, dc0, nc, sh0, dh0, nh = [int(x) for x in sl]
+    Vs, Vd = canon(src, S), canon(dst, Dp)
+    for so, do, _bo, s0, d0, n in np.asarray(reqs, dtype=np.int64).reshape(-1, 6):
+        if n == 0:
+            continue
+        sp, ss = _where(np.asarray(src_pt), so, s0, n, S.T)
+        dp, ds = _where(np.asarray(dst_pt), do, d0, n, Dp.T)
+        Vd[dl0:dl0 + nl, dp, dc0:dc0 + nc, ds, dh0:dh0 + nh, :] = \
+            Vs[sl0:sl0 + nl, sp, sc0:sc0 + nc, ss, sh0:sh0 + nh, :]

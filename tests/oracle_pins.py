@@ -456,9 +456,140 @@ def pin_tiny_workload(O):
     _same(back, got_buf, "tiny round trip")
 
 
+# ---------------------------------------------------------------------------
+# slices (layer range, kv range, head range)
+# ---------------------------------------------------------------------------
+
+def pin_slice_hand_example(O):
+    """Source: 2 layers, K and V, 4 heads, 8-element rows, one 2-token page.
+    Row (layer l, kv c, slot s, head h) holds 1000l + 100c + 10h + s.
+    Copy layer 1, V only, heads 2..3 into a 1-layer, 1-kv, 2-head pool whose
+    2-token page 0 starts at position 0.  Destination row (slot s, head h)
+    must hold 1000 + 100 + 10(2 + h) + s: 1120, 1130, 1121, 1131 in
+    [slot][head] order."""
+    S = PoolSpec(L=2, C=2, H=4, D=8, T=2, N=1, e=2, layout="LPCTHD")
+    Dp = PoolSpec(L=1, C=1, H=2, D=8, T=2, N=1, e=2, layout="LPCTHD")
+    src = np.zeros((2, 1, 2, 2, 4, 8), dtype="<u2")
+    for l, c, s_, h in itertools.product(range(2), range(2), range(2), range(4)):
+        src[l, 0, c, s_, h, :] = 1000 * l + 100 * c + 10 * h + s_
+    dst = np.zeros(Dp.elems, dtype="<u2")
+    err = O.transfer_slice(src.reshape(-1).view(np.uint8), S, dst.view(np.uint8), Dp,
+                           (1, 0, 1, 1, 0, 1, 2, 0, 2), [0], [0], [_req(n=2)])
+    assert err == 0
+    assert list(dst[::8]) == [1120, 1130, 1121, 1131], dst[::8]
+
+
+def _slice_case(O, ls, ld, Ts, Td, S_LCH, D_LCH, sl, seed):
+    rng = np.random.default_rng(seed)
+    (Ls, Cs, Hs), (Ld, Cd, Hd) = S_LCH, D_LCH
+    spec = [(Ts // 2 + 1, Td - 1, 3 * Ts + 1), (0, 1, 2 * Ts - 1), (Ts - 1, 0, 1)]
+    ks = [-(-(s0 + n) // Ts) for s0, _, n in spec]
+    kd = [-(-(d0 + n) // Td) for _, d0, n in spec]
+    S = PoolSpec(Ls, Cs, Hs, 8, T=Ts, N=sum(ks) + 3, e=2, layout=ls)
+    Dp = PoolSpec(Ld, Cd, Hd, 8, T=Td, N=sum(kd) + 3, e=2, layout=ld)
+    sp_, dp_ = rng.permutation(S.N).astype(np.int32), rng.permutation(Dp.N).astype(np.int32)
+    reqs, so, do = [], 0, 0
+    for (s0, d0, n), a, b in zip(spec, ks, kd):
+        reqs.append(_req(so=so, do=do, s0=s0, d0=d0, n=n))
+        so, do = so + a, do + b
+    src = _pool_bytes(S, seed)
+    dst = prefill_bytes(Dp.nbytes, 12)
+    exp = dst.copy()
+    npr.transfer_slice(src, S, exp, Dp, sl, sp_[:so], dp_[:do], reqs)
+    assert O.transfer_slice(src, S, dst, Dp, sl, sp_[:so], dp_[:do], reqs) == 0
+    _same(dst, exp, f"slice {sl} {ls}->{ld} T {Ts}->{Td}")
+
+
+def pin_slice_numpy(O):
+    """Layer, kv and head ranges at offsets on both sides, pools of different
+    layer / kv / head counts, every layout pair."""
+    cases = [((4, 2, 8), (2, 2, 4), (2, 0, 2, 0, 0, 2, 4, 0, 4)),     # TP=2 shard, layer stage
+             ((3, 2, 4), (3, 1, 4), (0, 0, 3, 1, 0, 1, 0, 0, 4)),     # V only
+             ((3, 2, 4), (5, 2, 6), (0, 2, 3, 0, 0, 2, 1, 3, 2)),     # into a larger pool
+             ((2, 1, 1), (2, 1, 3), (0, 0, 2, 0, 0, 1, 0, 2, 1))]     # one head into head 2
+    for i, (ls, ld) in enumerate(itertools.product(LAYOUTS, LAYOUTS)):
+        for j, (a, b, sl) in enumerate(cases):
+            _slice_case(O, ls, ld, 4, 8, a, b, sl, seed=500 + 10 * i + j)
+
+
+def pin_slice_decomposes_transfer(O):
+    """Full ranges equal the plain transfer; K then V, or one head half then
+    the other, or one layer half then the other, add up to it too."""
+    rng = np.random.default_rng(9)
+    L, C, H = 4, 2, 4
+    for ls, ld in (("LPCTHD", "PLCHTD"), ("LPCHTD", "LPCTHD")):
+        S = PoolSpec(L, C, H, 8, T=4, N=12, e=2, layout=ls)
+        Dp = PoolSpec(L, C, H, 8, T=8, N=8, e=2, layout=ld)
+        src = _pool_bytes(S, 3)
+        spt = rng.permutation(S.N).astype(np.int32)
+        dpt = rng.permutation(Dp.N).astype(np.int32)
+        reqs = [_req(so=0, do=0, s0=3, d0=5, n=20), _req(so=7, do=4, s0=0, d0=0, n=9)]
+        base = prefill_bytes(Dp.nbytes, 4)
+        full = base.copy()
+        assert O.transfer(src, S, full, Dp, spt, dpt, reqs) == 0
+        whole = base.copy()
+        assert O.transfer_slice(src, S, whole, Dp, (0, 0, L, 0, 0, C, 0, 0, H), spt, dpt, reqs) == 0
+        _same(whole, full, "full slice")
+        for parts in (((0, 0, L, 0, 0, 1, 0, 0, H), (0, 0, L, 1, 1, 1, 0, 0, H)),
+                      ((0, 0, L, 0, 0, C, 0, 0, 2), (0, 0, L, 0, 0, C, 2, 2, 2)),
+                      ((0, 0, 1, 0, 0, C, 0, 0, H), (1, 1, 3, 0, 0, C, 0, 0, H))):
+            acc = base.copy()
+            for sl in parts:
+                assert O.transfer_slice(src, S, acc, Dp, sl, spt, dpt, reqs) == 0
+            _same(acc, full, f"parts {parts}")
+
+
+def pin_slice_tp_roundtrip(O):
+    """8 heads split into two 4-head shards (one pool each), then merged back
+    into an 8-head pool: the result equals a plain transfer."""
+    rng = np.random.default_rng(2)
+    S = PoolSpec(2, 2, 8, 8, T=4, N=10, e=2, layout="LPCTHD")
+    half = PoolSpec(2, 2, 4, 8, T=8, N=6, e=2, layout="PLCHTD")
+    spt = rng.permutation(S.N).astype(np.int32)
+    hpt = rng.permutation(half.N).astype(np.int32)
+    reqs = [_req(so=0, do=0, s0=1, d0=0, n=30)]
+    back_reqs = [_req(so=0, do=0, s0=0, d0=1, n=30)]
+    src = _pool_bytes(S, 8)
+    shards = []
+    for h0 in (0, 4):
+        sh = prefill_bytes(half.nbytes, 5)
+        assert O.transfer_slice(src, S, sh, half, (0, 0, 2, 0, 0, 2, h0, 0, 4), spt, hpt, reqs) == 0
+        shards.append(sh)
+    merged = prefill_bytes(S.nbytes, 6)
+    mpt = rng.permutation(S.N).astype(np.int32)
+    for h0, sh in zip((0, 4), shards):
+        assert O.transfer_slice(sh, half, merged, S, (0, 0, 2, 0, 0, 2, 0, h0, 4), hpt, mpt,
+                                back_reqs) == 0
+    want = prefill_bytes(S.nbytes, 6)
+    # positions 1..30 of the source land at 1..30 of the merged pool
+    assert O.transfer(src, S, want, S, spt, mpt, [_req(so=0, do=0, s0=1, d0=1, n=30)]) == 0
+    _same(merged, want, "TP split and merge")
+
+
+
+def pin_slice_errors(O):
+    """The slice copy follows the same error rules as the plain transfer."""
+    S = PoolSpec(2, 2, 2, 8, T=4, N=4, e=2, layout="LPCTHD")
+    Dp = PoolSpec(1, 1, 2, 8, T=4, N=4, e=2, layout="LPCTHD")
+    src = random_bytes(S.nbytes, 1)
+    base = prefill_bytes(Dp.nbytes, 2)
+    sl = (1, 0, 1, 1, 0, 1, 0, 0, 2)
+    for spt, dpt, row, bits in (([0, 4], [0, 1], _req(n=8), ERR_SRC_PAGE),
+                                ([7, 1], [-1, 1], _req(n=4), ERR_DST_PAGE),
+                                ([0], [0, 1], _req(n=8), ERR_PT_RANGE),
+                                ([0, 1], [0, 1], _req(n=-2), ERR_BAD_REQ),
+                                ([0, 1], [2, 3], _req(s0=1, d0=2, n=5), 0)):
+        d = base.copy()
+        assert O.transfer_slice(src, S, d, Dp, sl, spt, dpt, [row]) == bits, (spt, dpt, row)
+        if bits == ERR_DST_PAGE or bits == ERR_BAD_REQ:
+            _same(d, base, "skipped positions written")
+
+
 PINS = [pin_hand_example, pin_hand_example_plchtd, pin_numpy_transfer,
         pin_numpy_transfer_widths, pin_numpy_gather_scatter, pin_identity_tables,
-        pin_roundtrip, pin_bijection, pin_errors, pin_max_position, pin_tiny_workload]
+        pin_roundtrip, pin_bijection, pin_errors, pin_max_position, pin_tiny_workload,
+        pin_slice_hand_example, pin_slice_numpy, pin_slice_decomposes_transfer,
+        pin_slice_tp_roundtrip, pin_slice_errors]
 
 
 def run_all(O) -> list:

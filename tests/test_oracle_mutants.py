@@ -77,7 +77,17 @@ MUTANTS = {
     "negative_start_accepted": ("return n >= 0 && start >= 0 &&", "return n >= 0 &&"),
     "int32_end_unchecked": ("&& start + n <= INT32_MAX;", ";"),
     "misaligned_block_accepted": ("if (off < 0 || (off * B->e) % 16 != 0)", "if (off < 0)"),
+    "slice_dst_layer_from_src_offset": ("sl[1] + l", "sl[0] + l"),
+    "slice_dst_head_from_src_offset": ("sl[7] + h", "sl[6] + h"),
+    "slice_src_kv_offset_dropped": ("sl[3] + c", "c"),
+    "slice_one_layer_short": ("l < sl[2]", "l + 1 < sl[2]"),
+    "slice_heads_of_the_pool": ("h < sl[8]", "h < S->H"),
 }
+# Sites that occur in both the pool -> pool and the slice copy: mutate one
+# occurrence at a time (0: ora_transfer, 1: ora_transfer_slice).
+SHARED = ("source_position_from_dst_start", "dst_position_from_src_start",
+          "source_resolved_first")
+CASES = sorted([(name, 0) for name in MUTANTS] + [(name, 1) for name in SHARED])
 
 
 def _run_pins(lib):
@@ -91,14 +101,18 @@ def test_real_oracle_passes_pins_in_child():
     assert r.returncode == 0, r.stdout + r.stderr
 
 
-@pytest.mark.parametrize("name", sorted(MUTANTS))
-def test_mutant_is_caught(name, tmp_path):
+@pytest.mark.parametrize("name,occurrence", CASES, ids=[f"{n}-{o}" for n, o in CASES])
+def test_mutant_is_caught(name, occurrence, tmp_path):
     old, new = MUTANTS[name]
     text = open(kvx_oracle.SOURCE).read()
-    assert text.count(old) == 1, f"mutation site for {name} must occur exactly once"
+    want = 2 if name in SHARED else 1
+    assert text.count(old) == want, f"mutation site for {name} must occur {want} time(s)"
     assert old != new
+    at = -1
+    for _ in range(occurrence + 1):
+        at = text.index(old, at + 1)
     src = tmp_path / "kvx_oracle_mutant.c"
-    src.write_text(text.replace(old, new))
+    src.write_text(text[:at] + new + text[at + len(old):])
     lib = str(tmp_path / "libkvx_oracle_mutant.so")
     kvx_oracle.build(str(src), lib)
     r = _run_pins(lib)
