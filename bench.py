@@ -8,8 +8,8 @@ role handoff:
 - 4096 x 64-token pools on both sides, layout [layer][page][kv][token][head][dim];
 - 32 requests with lengths uniform in [1024, 8192] on random page tables.
 A step is one fused kvx_transfer of all 32 requests.  ``--workload
-relayout|mla|host_tier`` selects the relayout, MLA partial-prefix and
-host-tier workloads.
+relayout|mla|host_tier|tp_reshard`` selects the relayout, MLA
+partial-prefix, host-tier and tensor-parallel reshard workloads.
 
 GB/s counts algorithmic bytes, GB = 1e9: every copied token position is read
 once and written once, 2 * tokens * L*C*H*D*e per step.
@@ -74,7 +74,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="handoff",
-                    choices=["handoff", "relayout", "mla", "host_tier"])
+                    choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard"])
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="layers of the workload the CPU oracle runs (0: skip)")
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
@@ -144,7 +144,10 @@ def main() -> int:
     def launch(d):
         st = d["st"]
         S, D = wl.sides[st.src], wl.sides[st.dst]
-        if st.op == "transfer":
+        if st.op == "transfer" and st.slice is not None:
+            kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["spt"], d["dpt"],
+                                   d["reqs"], errw)
+        elif st.op == "transfer":
             kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"], errw)
         elif st.op == "gather":
             kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, d["spt"], d["reqs"], errw)
@@ -255,9 +258,14 @@ def main() -> int:
         picks = sorted({round(i * (L - 1) / max(1, args.cpu_layers - 1))
                         for i in range(min(args.cpu_layers, L))})
         secs, moved, exact = 0.0, 0, True
+        if st.slice is not None:
+            L = st.slice[2]
+            picks = sorted({round(i * (L - 1) / max(1, args.cpu_layers - 1))
+                            for i in range(min(args.cpu_layers, L))})
         for l in picks:
-            r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l,
-                                                 wl.prefill_tag)
+            check = (layer_check.check_transfer_slice_layer if st.slice is not None
+                     else layer_check.check_transfer_layer)
+            r = check(mem[st.src], S, mem[st.dst], D, st, l, wl.prefill_tag)
             log(f"cpu oracle layer {l}: {r.oracle_seconds:.2f} s, bit-exact={r.equal}")
             secs += r.oracle_seconds
             moved += r.moved_bytes

@@ -151,6 +151,34 @@ int kvx_transfer(const kvx_pool *src, const kvx_pool *dst,
                  const kvx_req *reqs, int32_t n_reqs,
                  uint32_t *dev_err, void *stream);
 
+/* A layer range, a kv range and a head range, each at its own offset on
+ * either side (40 bytes).  Sec. 4.1.1: a view names a tuple of layers and a
+ * tuple of slices; Sec. 4.1.3: one node may hold the K half of a page and
+ * another the V half; Sec. 7: transfers between tensor-parallel layouts
+ * (a head range) and pipeline stages (a layer range). */
+typedef struct kvx_slice {
+    int32_t src_layer0, dst_layer0, num_layers;
+    int32_t src_kv0, dst_kv0, num_kv;
+    int32_t src_head0, dst_head0, num_heads;
+    int32_t reserved; /* must be 0 */
+} kvx_slice;
+
+/* Slice of a pool -> slice of another pool.  For every request record r,
+ * 0 <= i < n_tokens, l < num_layers, c < num_kv, h < num_heads and every d:
+ *   dst(dst_layer0 + l, dst_kv0 + c, dst_start + i, dst_head0 + h, d)
+ *     := src(src_layer0 + l, src_kv0 + c, src_start + i, src_head0 + h, d)
+ * The pools may differ in num_layers, num_kv and num_heads (and page size,
+ * page count and layout); head_dim and elem_bytes must match (else
+ * KVX_ERR_SHAPE).  Each range must lie inside its pool, counts must be
+ * >= 0 (KVX_ERR_RANGE otherwise); a zero count enqueues nothing.  Every
+ * other rule, argument and device error bit is that of kvx_transfer, which
+ * is this call with all ranges full and equal shapes. */
+int kvx_transfer_slice(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                       const int32_t *src_pt, int64_t src_pt_len,
+                       const int32_t *dst_pt, int64_t dst_pt_len,
+                       const kvx_req *reqs, int32_t n_reqs,
+                       uint32_t *dev_err, void *stream);
+
 /* Pool -> flat buffer: the offload (serialization) direction of Sec. 4.1.2. */
 int kvx_gather(const kvx_pool *src, const kvx_buf *dst,
                const int32_t *src_pt, int64_t src_pt_len,

@@ -87,6 +87,24 @@ def check_transfer_layer(src_t, S, dst_t, D, step, l: int, tag: int) -> LayerRes
     return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved)
 
 
+def check_transfer_slice_layer(src_t, S, dst_t, D, step, l: int, tag: int) -> LayerResult:
+    """Layer l of a slice transfer (l counts from the slice's first layer):
+    source layer src_layer0 + l lands in destination layer dst_layer0 + l."""
+    sl = list(step.slice)
+    ls, ld = sl[0] + l, sl[1] + l
+    s1, d1 = one_layer(S), one_layer(D)
+    src = pool_layer(src_t, S, ls)
+    got = pool_layer(dst_t, D, ld)
+    want = pool_layer_prefill(D, ld, tag)
+    one = [0, 0, 1] + sl[3:]
+    t0 = time.perf_counter()
+    err = kvx_oracle.default().transfer_slice(src, s1, want, d1, one, step.src_pt, step.dst_pt,
+                                               step.reqs)
+    dt = time.perf_counter() - t0
+    moved = 2 * int(step.reqs[:, 5].sum()) * sl[5] * sl[8] * S.D * S.e
+    return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved)
+
+
 def gather_scatter_layer(pool_before: np.ndarray, S, buf_t, B, pool_after: np.ndarray,
                          gather, scatter, l: int) -> tuple[bool, bool]:
     """Layer l of a gather (pool -> flat buffer) followed by a scatter (flat

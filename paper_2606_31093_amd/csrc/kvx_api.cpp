@@ -111,13 +111,15 @@ int device_view(const void *ptr, const char *name, void **dev_ptr) {
     return fail(KVX_ERR_RANGE, "%s (%p) is not device memory or mapped pinned host memory", name, ptr);
 }
 
-// Byte strides of (layer, page, kv, slot, head) for a pool layout.
-kvx::Side pool_side(const kvx_pool *p, void *base, const int32_t *pt, int64_t pt_len) {
+// Byte strides of (layer, page, kv, slot, head) for a pool layout, with the
+// base moved to (layer0, kv0, head0) of the range the call copies; `heads`
+// is how many heads it copies.
+kvx::Side pool_side(const kvx_pool *p, void *base, const int32_t *pt, int64_t pt_len,
+                    int32_t layer0, int32_t kv0, int32_t head0, int32_t heads) {
     const int64_t row = (int64_t)p->head_dim * p->elem_bytes;
     const int64_t L = p->num_layers, N = p->num_pages, C = p->num_kv, T = p->page_tokens,
                   H = p->num_heads;
     kvx::Side s{};
-    s.base = static_cast<char *>(base);
     const bool token_major = p->layout == KVX_LPCTHD || p->layout == KVX_PLCTHD;
     if (token_major) {
         s.s_h = row;
@@ -134,12 +136,14 @@ kvx::Side pool_side(const kvx_pool *p, void *base, const int32_t *pt, int64_t pt
         s.s_l = C * s.s_c;
         s.s_p = L * s.s_l;
     }
+    s.base = static_cast<char *>(base) + layer0 * s.s_l + kv0 * s.s_c + head0 * s.s_h;
     s.pt = pt;
     s.pt_len = pt_len;
     s.T = p->page_tokens;
     s.N = p->num_pages;
-    s.is_buf = 0;
-    s.tok_contig = token_major || H == 1;
+    // The copied heads of consecutive slots form one run when each slot's
+    // copied rows are adjacent and slots follow each other without a gap.
+    s.tok_contig = s.s_t == heads * row && (heads == 1 || s.s_h == row);
     s.cap_bytes = 0;
     return s;
 }
@@ -147,7 +151,6 @@ kvx::Side pool_side(const kvx_pool *p, void *base, const int32_t *pt, int64_t pt
 kvx::Side buf_side(const kvx_buf *b, void *base) {
     kvx::Side s{};
     s.base = static_cast<char *>(base);
-    s.is_buf = 1;
     s.tok_contig = 1;
     s.T = 1;
     s.N = 0;
@@ -230,6 +233,7 @@ int view_all(const void *src, const void *dst, const int32_t *src_pt, int64_t sr
     return KVX_OK;
 }
 
+// `s` gives the layers, kv components and heads the call copies.
 void finish_params(kvx::Params &P, const Shape &s, const Views &v, int32_t n_reqs) {
     P.reqs = v.reqs;
     P.err = v.err;
@@ -247,7 +251,6 @@ void finish_params(kvx::Params &P, const Shape &s, const Views &v, int32_t n_req
     P.fd_H = kvx::make_fastdiv((uint32_t)P.H);
     P.fd_Tt = kvx::make_fastdiv((uint32_t)ts.T);
     P.fd_To = kvx::make_fastdiv((uint32_t)os.T);
-    P.fd_HV = kvx::make_fastdiv((uint32_t)(P.H * P.vpr));
 }
 
 int enqueue(const kvx::Params &P, void *stream) {
@@ -257,6 +260,64 @@ int enqueue(const kvx::Params &P, void *stream) {
     return KVX_OK;
 }
 
+// A slice's ranges must lie inside both pools; rows must have the same
+// width on both sides.
+int check_slice(const kvx_slice &sl, const Shape &s, const Shape &d) {
+    if (s.D != d.D || s.e != d.e)
+        return fail(KVX_ERR_SHAPE, "head_dim/elem_bytes differ: (%d, %d) vs (%d, %d)", s.D, s.e,
+                    d.D, d.e);
+    if (sl.reserved != 0) return fail(KVX_ERR_RANGE, "slice: reserved field must be 0");
+    const struct {
+        const char *what;
+        int32_t s0, d0, n, smax, dmax;
+    } r[3] = {{"layer", sl.src_layer0, sl.dst_layer0, sl.num_layers, s.L, d.L},
+              {"kv", sl.src_kv0, sl.dst_kv0, sl.num_kv, s.C, d.C},
+              {"head", sl.src_head0, sl.dst_head0, sl.num_heads, s.H, d.H}};
+    for (const auto &x : r) {
+        if (x.n < 0 || x.s0 < 0 || x.d0 < 0 || (int64_t)x.s0 + x.n > x.smax ||
+            (int64_t)x.d0 + x.n > x.dmax)
+            return fail(KVX_ERR_RANGE,
+                        "slice %s range: src [%d, %lld) of %d, dst [%d, %lld) of %d", x.what, x.s0,
+                        (long long)x.s0 + x.n, x.smax, x.d0, (long long)x.d0 + x.n, x.dmax);
+    }
+    return KVX_OK;
+}
+
+// Pool -> pool; slice == NULL copies everything between equal shapes.
+int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                  const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
+                  int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err,
+                  void *stream) {
+    g_last_error.clear();
+    Shape ss, ds;
+    int st;
+    if ((st = check_pool(src, "src", ss))) return st;
+    if ((st = check_pool(dst, "dst", ds))) return st;
+    kvx_slice sl;
+    if (slice) {
+        sl = *slice;
+        if ((st = check_slice(sl, ss, ds))) return st;
+    } else {
+        if ((st = same_shape(ss, ds))) return st;
+        sl = kvx_slice{0, 0, ss.L, 0, 0, ss.C, 0, 0, ss.H, 0};
+    }
+    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
+    if ((st = check_table(src_pt, src_pt_len, "src_pt"))) return st;
+    if ((st = check_table(dst_pt, dst_pt_len, "dst_pt"))) return st;
+    if (n_reqs == 0 || sl.num_layers == 0 || sl.num_kv == 0 || sl.num_heads == 0) return KVX_OK;
+    Views v;
+    if ((st = view_all(src->base, dst->base, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, dev_err, v)))
+        return st;
+    kvx::Params P{};
+    P.op = kvx::OP_TRANSFER;
+    P.src = pool_side(src, v.src, v.src_pt, src_pt_len, sl.src_layer0, sl.src_kv0, sl.src_head0,
+                      sl.num_heads);
+    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, sl.dst_layer0, sl.dst_kv0, sl.dst_head0,
+                      sl.num_heads);
+    finish_params(P, Shape{sl.num_layers, sl.num_kv, sl.num_heads, ss.D, ss.e}, v, n_reqs);
+    return enqueue(P, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -264,25 +325,18 @@ extern "C" {
 int kvx_transfer(const kvx_pool *src, const kvx_pool *dst, const int32_t *src_pt, int64_t src_pt_len,
                  const int32_t *dst_pt, int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs,
                  uint32_t *dev_err, void *stream) {
+    return transfer_impl(src, dst, nullptr, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
+                         dev_err, stream);
+}
+
+int kvx_transfer_slice(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                       const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
+                       int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err,
+                       void *stream) {
     g_last_error.clear();
-    Shape ss, ds;
-    int st;
-    if ((st = check_pool(src, "src", ss))) return st;
-    if ((st = check_pool(dst, "dst", ds))) return st;
-    if ((st = same_shape(ss, ds))) return st;
-    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
-    if ((st = check_table(src_pt, src_pt_len, "src_pt"))) return st;
-    if ((st = check_table(dst_pt, dst_pt_len, "dst_pt"))) return st;
-    if (n_reqs == 0) return KVX_OK;
-    Views v;
-    if ((st = view_all(src->base, dst->base, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, dev_err, v)))
-        return st;
-    kvx::Params P{};
-    P.op = kvx::OP_TRANSFER;
-    P.src = pool_side(src, v.src, v.src_pt, src_pt_len);
-    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len);
-    finish_params(P, ss, v, n_reqs);
-    return enqueue(P, stream);
+    if (!slice) return fail(KVX_ERR_NULL, "slice is NULL");
+    return transfer_impl(src, dst, slice, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
+                         dev_err, stream);
 }
 
 int kvx_gather(const kvx_pool *src, const kvx_buf *dst, const int32_t *src_pt, int64_t src_pt_len,
@@ -301,7 +355,7 @@ int kvx_gather(const kvx_pool *src, const kvx_buf *dst, const int32_t *src_pt, i
         return st;
     kvx::Params P{};
     P.op = kvx::OP_GATHER;
-    P.src = pool_side(src, v.src, v.src_pt, src_pt_len);
+    P.src = pool_side(src, v.src, v.src_pt, src_pt_len, 0, 0, 0, ss.H);
     P.dst = buf_side(dst, v.dst);
     finish_params(P, ss, v, n_reqs);
     return enqueue(P, stream);
@@ -324,7 +378,7 @@ int kvx_scatter(const kvx_buf *src, const kvx_pool *dst, const int32_t *dst_pt, 
     kvx::Params P{};
     P.op = kvx::OP_SCATTER;
     P.src = buf_side(src, v.src);
-    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len);
+    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, 0, 0, 0, ds.H);
     finish_params(P, ss, v, n_reqs);
     return enqueue(P, stream);
 }

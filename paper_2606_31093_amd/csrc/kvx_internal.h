@@ -37,10 +37,11 @@ __host__ __device__ inline uint32_t fd_div(const FastDiv &f, uint32_t n) {
 }
 
 // One side of a copy.  A pool side addresses row (l, page, c, slot, h) at
-// base + l*s_l + page*s_p + c*s_c + slot*s_t + h*s_h (bytes); a buffer side
-// addresses row (l, c, i, h) of a request's block at
-// base + 16*blk + ((l*C + c)*n + i)*H*row + h*row, with blk the block's
-// offset in 16-byte units.
+// base + l*s_l + page*s_p + c*s_c + slot*s_t + h*s_h (bytes), with base
+// already moved to the first layer, kv component and head the call copies;
+// a buffer side addresses row (l, c, i, h) of a request's block at
+// base + blk + ((l*C + c)*n + i)*H*row + h*row, with blk the block's byte
+// offset.
 struct Side {
     char *base;
     int64_t s_l, s_p, s_c, s_t, s_h;
@@ -48,8 +49,7 @@ struct Side {
     int64_t pt_len;
     int32_t T;        // tokens per page (pool side)
     int32_t N;        // pages (pool side)
-    int32_t is_buf;   // 1 for a flat buffer side
-    int32_t tok_contig;  // rows of consecutive slots, all heads, are adjacent
+    int32_t tok_contig;  // rows of consecutive slots, all copied heads, are adjacent
     int64_t cap_bytes;   // buffer side: bytes addressable from base
 };
 
@@ -61,12 +61,12 @@ struct Params {
     uint32_t *err;
     int32_t n_reqs;
     int32_t op;
-    int32_t L, C, H;
+    int32_t L, C, H;     // layers, kv components and heads copied
     int32_t row_bytes;   // head_dim * elem_bytes, a multiple of 16
     int32_t vpr;         // 16-byte vectors per row
     int32_t elem_bytes;
     int32_t flat;        // both sides tok_contig: a tile is C contiguous runs per piece
-    FastDiv fd_vpr, fd_H, fd_Tt, fd_To, fd_HV;
+    FastDiv fd_vpr, fd_H, fd_Tt, fd_To;
 };
 
 // Launch on `stream`; returns a hipError_t value.

@@ -50,18 +50,6 @@
 #ifndef KVX_BLOCK
 #define KVX_BLOCK 256
 #endif
-#ifndef KVX_WAVE_CONTIG
-#define KVX_WAVE_CONTIG 0
-#endif
-#ifndef KVX_PIPE
-#define KVX_PIPE 0
-#endif
-#ifndef KVX_ROTATE
-#define KVX_ROTATE 0   // start each tile's vector stream at a per-workgroup 1 KiB offset
-#endif
-#ifndef KVX_PAGE_FASTEST
-#define KVX_PAGE_FASTEST 0   // tile order within a request: 0 layer fastest, 1 page fastest
-#endif
 
 namespace kvx {
 namespace {
@@ -96,7 +84,6 @@ struct Req {
     int64_t t_pt_off, o_pt_off;  // table offsets of the tiling / other side
     int64_t blk;                 // buffer block offset in bytes
     int64_t tiles;               // tiles this request contributes
-    int64_t pages;               // tiling-side pages this request touches
     int32_t t_start, o_start, n;
     int32_t j0;                  // first tiling-side page (logical)
 };
@@ -132,15 +119,13 @@ __device__ __forceinline__ bool load_req(const Params &p, int32_t r, Req &q) {
     const Side &ts = tsrc ? p.src : p.dst;
     if (n == 0) {
         q.tiles = 0;
-        q.pages = 0;
         q.j0 = 0;
         return true;
     }
     const int32_t j0 = q.t_start / ts.T;
     const int32_t j1 = (q.t_start + n - 1) / ts.T;
     q.j0 = j0;
-    q.pages = j1 - j0 + 1;
-    q.tiles = q.pages * p.L;
+    q.tiles = (int64_t)(j1 - j0 + 1) * p.L;
     return true;
 }
 
@@ -149,86 +134,14 @@ template <int U>
 __device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, int64_t s_sc,
                                           uint32_t R, int32_t C) {
     const uint32_t total = R * (uint32_t)C;
-#if KVX_WAVE_CONTIG
-    // each wavefront streams U consecutive 1 KiB blocks per iteration
-    const uint32_t lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
-    for (uint32_t base = wid * U * kWave + lane; base < total; base += kBlock * U) {
-        v4u v[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t k = base + u * kWave;
-            if (k < total) {
-                const uint32_t c = k >= R;
-                v[u] = ld16(s + c * s_sc + (int64_t)(k - c * R) * 16);
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t k = base + u * kWave;
-            if (k < total) {
-                const uint32_t c = k >= R;
-                st16(d + c * d_sc + (int64_t)(k - c * R) * 16, v[u]);
-            }
-        }
-    }
-    return;
-#endif
-#if KVX_PIPE
-    // loads of the next group are issued before the stores of this one
-    {
-        v4u cur[U], nxt[U];
-        uint32_t k0 = threadIdx.x;
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const uint32_t k = k0 + u * kBlock;
-            if (k < total) {
-                const uint32_t c = k >= R;
-                cur[u] = ld16(s + c * s_sc + (int64_t)(k - c * R) * 16);
-            }
-        }
-        for (; k0 < total; k0 += kBlock * U) {
-            const uint32_t k1 = k0 + kBlock * U;
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t k = k1 + u * kBlock;
-                if (k < total) {
-                    const uint32_t c = k >= R;
-                    nxt[u] = ld16(s + c * s_sc + (int64_t)(k - c * R) * 16);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) {
-                const uint32_t k = k0 + u * kBlock;
-                if (k < total) {
-                    const uint32_t c = k >= R;
-                    st16(d + c * d_sc + (int64_t)(k - c * R) * 16, cur[u]);
-                }
-            }
-#pragma unroll
-            for (int u = 0; u < U; ++u) cur[u] = nxt[u];
-        }
-    }
-    return;
-#endif
-#if KVX_ROTATE
-    // Rotate the stream so that workgroups working on equally aligned runs
-    // do not sweep the same address phase at the same time.
-    const uint32_t rot = total >= 2 * kWave
-                             ? ((blockIdx.x * 2654435761u) >> 7) % (total / kWave) * kWave
-                             : 0;
-#else
-    const uint32_t rot = 0;
-#endif
     for (uint32_t k0 = threadIdx.x; k0 < total; k0 += kBlock * U) {
         v4u v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const uint32_t k = k0 + u * kBlock;
             if (k < total) {
-                uint32_t kr = k + rot;
-                kr = kr >= total ? kr - total : kr;
-                const uint32_t c = kr >= R;
-                const uint32_t w = kr - c * R;
+                const uint32_t c = k >= R;
+                const uint32_t w = k - c * R;
                 v[u] = ld16(s + c * s_sc + (int64_t)w * 16);
             }
         }
@@ -236,10 +149,8 @@ __device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, 
         for (int u = 0; u < U; ++u) {
             const uint32_t k = k0 + u * kBlock;
             if (k < total) {
-                uint32_t kr = k + rot;
-                kr = kr >= total ? kr - total : kr;
-                const uint32_t c = kr >= R;
-                const uint32_t w = kr - c * R;
+                const uint32_t c = k >= R;
+                const uint32_t w = k - c * R;
                 st16(d + c * d_sc + (int64_t)w * 16, v[u]);
             }
         }
@@ -347,14 +258,8 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
     const Side &os = kTileSrc ? p.dst : p.src;
 
     Tile t;
-#if KVX_PAGE_FASTEST
-    const int64_t lq = local / q.pages;
-    const int64_t jj = local - lq * q.pages;
-    t.l = (int32_t)lq;
-#else
     const int64_t jj = local / p.L;
     t.l = (int32_t)(local - jj * p.L);
-#endif
     const int64_t j = q.j0 + jj;
     const int64_t page_lo = j * ts.T;
     const int64_t qa = page_lo > q.t_start ? page_lo : q.t_start;

@@ -3,8 +3,8 @@
 Every step of the copy runs in the library's HIP kernels.  PyTorch supplies
 device memory and the stream: tensors are passed as raw pointers and the
 kernels run on ``torch.cuda.current_stream()`` unless a stream is given.
-The functions keep the C names: ``kvx_transfer``, ``kvx_gather`` and
-``kvx_scatter``.  A missing or unloadable library raises; there is no
+The functions keep the C names: ``kvx_transfer``, ``kvx_transfer_slice``,
+``kvx_gather`` and ``kvx_scatter``.  A missing or unloadable library raises; there is no
 fallback path.
 
 Pool and buffer shapes are duck-typed: a pool shape has integer attributes
@@ -51,6 +51,23 @@ class Buf(ctypes.Structure):
                 ("reserved", ctypes.c_int32), ("capacity_elems", ctypes.c_int64)]
 
 
+class Slice(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int32) for k in (
+        "src_layer0", "dst_layer0", "num_layers", "src_kv0", "dst_kv0", "num_kv",
+        "src_head0", "dst_head0", "num_heads", "reserved")]
+
+
+def slice_desc(sl) -> Slice:
+    """A kvx_slice from (src_layer0, dst_layer0, num_layers, src_kv0, dst_kv0,
+    num_kv, src_head0, dst_head0, num_heads)."""
+    if isinstance(sl, Slice):
+        return sl
+    vals = [int(x) for x in sl]
+    if len(vals) != 9:
+        raise ValueError("a slice has nine fields")
+    return Slice(*vals, 0)
+
+
 class KvxError(RuntimeError):
     def __init__(self, status: int, message: str):
         super().__init__(f"{STATUS.get(status, status)}: {message}")
@@ -77,9 +94,11 @@ def lib() -> ctypes.CDLL:
         vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         pp, bp = ctypes.POINTER(Pool), ctypes.POINTER(Buf)
         L.kvx_transfer.argtypes = [pp, pp, vp, i64, vp, i64, vp, i32, vp, vp]
+        L.kvx_transfer_slice.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp, i32,
+                                         vp, vp]
         L.kvx_gather.argtypes = [pp, bp, vp, i64, vp, i32, vp, vp]
         L.kvx_scatter.argtypes = [bp, pp, vp, i64, vp, i32, vp, vp]
-        for f in (L.kvx_transfer, L.kvx_gather, L.kvx_scatter):
+        for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_gather, L.kvx_scatter):
             f.restype = ctypes.c_int
         L.kvx_pool_bytes.argtypes = [pp]
         L.kvx_pool_bytes.restype = ctypes.c_int64
@@ -203,6 +222,18 @@ def kvx_transfer(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, dev_err=Non
     _check(lib().kvx_transfer(ctypes.byref(S), ctypes.byref(D), _ptr(src_pt), _len(src_pt),
                               _ptr(dst_pt), _len(dst_pt), _ptr(reqs), _n_reqs(reqs),
                               _ptr(dev_err), _stream(stream)))
+
+
+def kvx_transfer_slice(src, src_spec, dst, dst_spec, sl, src_pt, dst_pt, reqs, dev_err=None,
+                       stream=None) -> None:
+    """Slice of a pool -> slice of another pool (see kvx_transfer_slice in
+    include/kvx.h).  ``sl`` is a ``Slice`` or the nine range fields."""
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    S, D, X = pool_desc(src_spec, src), pool_desc(dst_spec, dst), slice_desc(sl)
+    _check(lib().kvx_transfer_slice(ctypes.byref(S), ctypes.byref(D), ctypes.byref(X),
+                                    _ptr(src_pt), _len(src_pt), _ptr(dst_pt), _len(dst_pt),
+                                    _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
 
 
 def kvx_gather(src, src_spec, dst, buf_spec, src_pt, reqs, dev_err=None, stream=None) -> None:

@@ -90,6 +90,7 @@ class Step:
     src_pt: np.ndarray | None    # int32 page table of a pool source
     dst_pt: np.ndarray | None    # int32 page table of a pool destination
     reqs: np.ndarray             # (n, 6) int64 request records
+    slice: tuple | None = None   # transfer of a layer/kv/head range: nine fields
 
     @property
     def n_tokens(self) -> int:
@@ -109,7 +110,11 @@ class Workload:
 
     def algorithmic_bytes(self, step: Step) -> int:
         """Payload read plus payload written by one step: every copied token
-        position moves token_bytes once in and once out."""
+        position moves its copied rows once in and once out."""
+        if step.slice is not None:
+            S = self.sides[step.src]
+            nl, nc, nh = step.slice[2], step.slice[5], step.slice[8]
+            return 2 * step.n_tokens * nl * nc * nh * S.D * S.e
         return 2 * step.n_tokens * self.sides[step.src].token_bytes
 
 
@@ -253,7 +258,29 @@ def host_tier(small: bool = False) -> Workload:
                     value_seed=2005, prefill_tag=5, host_sides=("buf",))
 
 
-NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier")
+def tp_reshard(small: bool = False) -> Workload:
+    """Tensor-parallel reshard of the handoff cache: a consumer running with
+    two tensor-parallel ranks holds 4 of the 8 KV heads per pool; this moves
+    heads [4, 8) of every layer of the 32 handoff requests into its 4-head
+    pool (Sec. 7: transfers across tensor-parallel configurations; Sec. 4.1.1:
+    views over slice tuples)."""
+    if small:
+        rng = np.random.default_rng(1106)
+        L, H, N, nreq, lo, hi = 3, 4, 64, 4, 1, 700
+    else:
+        rng = np.random.default_rng(1006)
+        L, H, N, nreq, lo, hi = 36, 8, 4096, 32, 1024, 8192
+    src = PoolSpec(L, 2, H, 128, T=64, N=N, e=2, layout="LPCTHD")
+    dst = PoolSpec(L, 2, H // 2, 128, T=64, N=N, e=2, layout="LPCTHD")
+    lengths = rng.integers(lo, hi + 1, size=nreq)
+    wl = _transfer_workload("tp_reshard", 6, f"TP reshard {L}L x heads [{H // 2}, {H}) of {H} x 128 "
+                            f"-> {H // 2}-head pool, 64-token pages, {nreq} requests",
+                            src, dst, lengths, [0] * nreq, rng)
+    wl.steps[0].slice = (0, 0, L, 0, 0, 2, H // 2, 0, H // 2)
+    return wl
+
+
+NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier", "tp_reshard")
 
 
 def get(name: str, small: bool = False) -> Workload:
@@ -261,7 +288,7 @@ def get(name: str, small: bool = False) -> Workload:
     if name == "tiny":
         return tiny()
     return {"handoff": handoff, "relayout": relayout, "mla": mla,
-            "host_tier": host_tier}[name](small=small)
+            "host_tier": host_tier, "tp_reshard": tp_reshard}[name](small=small)
 
 
 def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:

@@ -86,3 +86,32 @@ def layout_matrix():
     """Every (source layout, destination layout, T_src, T_dst)."""
     for (ls, ld), (Ts, Td) in itertools.product(itertools.product(LAYOUTS, LAYOUTS), T_PAIRS):
         yield ls, ld, Ts, Td
+
+
+def slice_case(ls, ld, Ts, Td, S_LCH, D_LCH, sl, seed, *, D=8, e=2) -> Workload:
+    """Slice of one pool into another of a different layer/kv/head count."""
+    rng = np.random.default_rng(seed)
+    (Ls, Cs, Hs), (Ld, Cd, Hd) = S_LCH, D_LCH
+    spec = [(Ts // 2 + 1, Td - 1, 3 * Ts + 1), (0, 1, 2 * Ts - 1), (Ts - 1, 0, 1), (0, 0, 0)]
+    ks = [_cdiv(s0 + n, Ts) for s0, _, n in spec]
+    kd = [_cdiv(d0 + n, Td) for _, d0, n in spec]
+    S = PoolSpec(Ls, Cs, Hs, D, T=Ts, N=sum(ks) + 3, e=e, layout=ls)
+    Dp = PoolSpec(Ld, Cd, Hd, D, T=Td, N=sum(kd) + 3, e=e, layout=ld)
+    sperm, dperm = rng.permutation(S.N).astype(np.int32), rng.permutation(Dp.N).astype(np.int32)
+    rows, so, do = [], 0, 0
+    for (s0, d0, n), a, b in zip(spec, ks, kd):
+        rows.append([so, do, 0, s0, d0, n])
+        so, do = so + a, do + b
+    step = Step("transfer", "A", "B", sperm[:so], dperm[:do], np.asarray(rows, np.int64),
+                slice=tuple(sl))
+    return Workload("case", f"slice {sl} {ls}/T{Ts} {S_LCH} -> {ld}/T{Td} {D_LCH}",
+                    {"A": S, "B": Dp}, [step], value_seed=seed, prefill_tag=seed & 0xFF)
+
+
+SLICES = [((4, 2, 8), (2, 2, 4), (2, 0, 2, 0, 0, 2, 4, 0, 4)),     # TP=2 shard of a layer stage
+          ((3, 2, 4), (3, 1, 4), (0, 0, 3, 1, 0, 1, 0, 0, 4)),     # V only
+          ((3, 2, 4), (3, 1, 4), (0, 0, 3, 0, 0, 1, 0, 0, 4)),     # K only
+          ((3, 2, 4), (5, 2, 6), (0, 2, 3, 0, 0, 2, 1, 3, 2)),     # into a larger pool
+          ((2, 1, 1), (2, 1, 3), (0, 0, 2, 0, 0, 1, 0, 2, 1)),     # one head into head 2
+          ((2, 2, 4), (2, 2, 4), (0, 0, 2, 0, 0, 2, 0, 0, 4)),     # everything
+          ((2, 2, 8), (2, 2, 8), (1, 0, 1, 1, 0, 1, 3, 5, 1))]     # one row per token

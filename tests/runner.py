@@ -31,7 +31,9 @@ def run_oracle(wl, init: dict, reqs_override=None) -> tuple[dict, list]:
     for i, st in enumerate(wl.steps):
         reqs = st.reqs if reqs_override is None else reqs_override[i]
         S, D = wl.sides[st.src], wl.sides[st.dst]
-        if st.op == "transfer":
+        if st.op == "transfer" and st.slice is not None:
+            e = O.transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, st.src_pt, st.dst_pt, reqs)
+        elif st.op == "transfer":
             e = O.transfer(mem[st.src], S, mem[st.dst], D, st.src_pt, st.dst_pt, reqs)
         elif st.op == "gather":
             e = O.gather(mem[st.src], S, mem[st.dst], D, st.src_pt, reqs)
@@ -68,7 +70,9 @@ def run_gpu(wl, init: dict, raw_reqs=None) -> tuple[dict, list]:
         S, D = wl.sides[st.src], wl.sides[st.dst]
         spt = kvx.device_table(st.src_pt, dev) if st.src_pt is not None else None
         dpt = kvx.device_table(st.dst_pt, dev) if st.dst_pt is not None else None
-        if st.op == "transfer":
+        if st.op == "transfer" and st.slice is not None:
+            kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, spt, dpt, reqs, err)
+        elif st.op == "transfer":
             kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs, err)
         elif st.op == "gather":
             kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, spt, reqs, err)

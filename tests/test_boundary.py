@@ -68,6 +68,11 @@ int main(void) {
   F(kvx_buf, head_dim); F(kvx_buf, elem_bytes); F(kvx_buf, reserved); F(kvx_buf, capacity_elems);
   F(kvx_req, src_pt_off); F(kvx_req, dst_pt_off); F(kvx_req, buf_off); F(kvx_req, src_start);
   F(kvx_req, dst_start); F(kvx_req, n_tokens); F(kvx_req, reserved);
+  printf("kvx_slice %zu\n", sizeof(kvx_slice));
+  F(kvx_slice, src_layer0); F(kvx_slice, dst_layer0); F(kvx_slice, num_layers);
+  F(kvx_slice, src_kv0); F(kvx_slice, dst_kv0); F(kvx_slice, num_kv);
+  F(kvx_slice, src_head0); F(kvx_slice, dst_head0); F(kvx_slice, num_heads);
+  F(kvx_slice, reserved);
   return 0;
 }''')
     exe = tmp_path / "layout"
@@ -86,6 +91,9 @@ int main(void) {
         assert got[f"kvx_buf.{name}"] == getattr(kvx.Buf, name).offset
     for name in kvx.REQ_DTYPE.names:
         assert got[f"kvx_req.{name}"] == kvx.REQ_DTYPE.fields[name][1]
+    assert got["kvx_slice"] == ctypes.sizeof(kvx.Slice)
+    for name, _ in kvx.Slice._fields_:
+        assert got[f"kvx_slice.{name}"] == getattr(kvx.Slice, name).offset
 
 
 def test_strerror(lib):
@@ -164,6 +172,43 @@ def test_gather_scatter_host_validation(lib):
     assert L.kvx_gather(ctypes.byref(sp), ctypes.byref(wrong), FAKE, 1, FAKE, 1, None, None) == -2
     assert L.kvx_gather(None, ctypes.byref(bd), FAKE, 1, FAKE, 1, None, None) == -1
     assert L.kvx_scatter(ctypes.byref(bd), None, FAKE, 1, FAKE, 1, None, None) == -1
+
+
+def _call_slice(S, D, sl, n_reqs=1, **kw):
+    L = kvx.lib()
+    sp, dp = kvx.pool_desc(S, FAKE), kvx.pool_desc(D, FAKE)
+    x = sl if sl is None else kvx.slice_desc(sl)
+    return L.kvx_transfer_slice(ctypes.byref(sp), ctypes.byref(dp),
+                                None if x is None else ctypes.byref(x), FAKE, 1, FAKE, 1,
+                                FAKE, n_reqs, None, None)
+
+
+BIG = PoolSpec(4, 2, 8, 64, T=16, N=8, e=2, layout="LPCTHD")
+SMALL = PoolSpec(2, 1, 4, 64, T=32, N=8, e=2, layout="PLCHTD")
+
+
+@pytest.mark.parametrize("S,D,sl,n_reqs,status", [
+    (BIG, SMALL, (2, 0, 2, 1, 0, 1, 4, 0, 4), 0, 0),              # valid: nothing to enqueue
+    (BIG, SMALL, (2, 0, 2, 1, 0, 0, 4, 0, 4), 1, 0),              # zero kv count: nothing to do
+    (BIG, SMALL, None, 1, -1),                                      # NULL slice
+    (BIG, SMALL, (3, 0, 2, 0, 0, 1, 0, 0, 4), 1, -5),             # layers past the source
+    (BIG, SMALL, (0, 1, 2, 0, 0, 1, 0, 0, 4), 1, -5),             # layers past the destination
+    (BIG, SMALL, (0, 0, 2, 0, 0, 2, 0, 0, 4), 1, -5),             # two kv into a one-kv pool
+    (BIG, SMALL, (0, 0, 2, 0, 0, 1, 6, 0, 4), 1, -5),             # heads past the source
+    (BIG, SMALL, (0, 0, 2, 0, 0, 1, 0, 1, 4), 1, -5),             # heads past the destination
+    (BIG, SMALL, (0, 0, -1, 0, 0, 1, 0, 0, 4), 1, -5),            # negative count
+    (BIG, SMALL, (-1, 0, 1, 0, 0, 1, 0, 0, 4), 1, -5),            # negative offset
+    (BIG, PoolSpec(2, 1, 4, 32, T=32, N=8, e=2), (0, 0, 1, 0, 0, 1, 0, 0, 1), 1, -2),  # head_dim
+    (BIG, PoolSpec(2, 1, 4, 64, T=32, N=8, e=4), (0, 0, 1, 0, 0, 1, 0, 0, 1), 1, -2),  # elem size
+])
+def test_slice_host_validation(lib, S, D, sl, n_reqs, status):
+    assert _call_slice(S, D, sl, n_reqs) == status
+
+
+def test_slice_reserved_must_be_zero(lib):
+    x = kvx.slice_desc((0, 0, 1, 0, 0, 1, 0, 0, 1))
+    x.reserved = 3
+    assert _call_slice(BIG, SMALL, x) == -5
 
 
 def test_last_error_is_per_call(lib):

@@ -36,7 +36,10 @@ def _run(torch, wl, mem, d):
     st = d["st"]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     S, D = wl.sides[st.src], wl.sides[st.dst]
-    if st.op == "transfer":
+    if st.op == "transfer" and st.slice is not None:
+        kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["spt"], d["dpt"],
+                               d["reqs"], err)
+    elif st.op == "transfer":
         kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"], err)
     elif st.op == "gather":
         kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, d["spt"], d["reqs"], err)
@@ -51,7 +54,7 @@ def _free(torch, *objs):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("k", ["handoff", "relayout", "mla"])
+@pytest.mark.parametrize("k", ["handoff", "relayout", "mla", "tp_reshard"])
 def test_full_transfer(torch, k):
     from oracle import layer_check
     wl, mem, dsteps = _setup(torch, k)
@@ -63,8 +66,14 @@ def test_full_transfer(torch, k):
         assert _run(torch, wl, mem, dsteps[0]) == 0
     assert int(src.view(torch.int64).sum().item()) == before, "source pool modified"
     S, D = wl.sides[st.src], wl.sides[st.dst]
-    for l in sorted({0, S.L // 2, S.L - 1}):
-        r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l, wl.prefill_tag)
+    n_layers = st.slice[2] if st.slice is not None else S.L
+    for l in sorted({0, n_layers // 2, n_layers - 1}):
+        if st.slice is not None:
+            r = layer_check.check_transfer_slice_layer(mem[st.src], S, mem[st.dst], D, st, l,
+                                                       wl.prefill_tag)
+        else:
+            r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l,
+                                                 wl.prefill_tag)
         print(f"  layer {l}: oracle {r.oracle_seconds:.2f} s, equal={r.equal}", flush=True)
         assert r.equal, f"{k} layer {l} differs from the oracle"
     _free(torch, mem, dsteps)

@@ -78,6 +78,61 @@ def test_many_requests_and_empty_ones():
 
 
 # ---------------------------------------------------------------------------
+# slices (layer range, kv range, head range)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("ls,ld", [("LPCTHD", "LPCTHD"), ("LPCTHD", "PLCHTD"), ("LPCHTD", "LPCHTD"),
+                                   ("PLCTHD", "LPCHTD"), ("PLCHTD", "PLCTHD")])
+@pytest.mark.parametrize("k", range(len(cases.SLICES)))
+@pytest.mark.parametrize("Ts,Td", [(4, 8), (16, 16), (1, 32)])
+def test_slices(ls, ld, k, Ts, Td):
+    a, b, sl = cases.SLICES[k]
+    check(cases.slice_case(ls, ld, Ts, Td, a, b, sl, seed=k * 97 + Ts * 7 + Td))
+
+
+def test_slice_wide_rows():
+    check(cases.slice_case("LPCTHD", "LPCTHD", 64, 64, (3, 1, 1), (2, 1, 1),
+                           (1, 0, 2, 0, 0, 1, 0, 0, 1), seed=4, D=576))
+
+
+def test_tp_split_and_merge():
+    """Eight heads split into two four-head shards, then merged back."""
+    S = PoolSpec(2, 2, 8, 64, T=16, N=12, e=2, layout="LPCTHD")
+    half = PoolSpec(2, 2, 4, 64, T=32, N=6, e=2, layout="PLCHTD")
+    rng = np.random.default_rng(3)
+    spt = rng.permutation(S.N).astype(np.int32)
+    hpt = rng.permutation(half.N).astype(np.int32)
+    mpt = rng.permutation(S.N).astype(np.int32)
+    r1 = np.asarray([[0, 0, 0, 5, 0, 100]], np.int64)
+    r2 = np.asarray([[0, 0, 0, 0, 5, 100]], np.int64)
+    steps = [Step("transfer", "A", "H0", spt, hpt, r1, slice=(0, 0, 2, 0, 0, 2, 0, 0, 4)),
+             Step("transfer", "A", "H1", spt, hpt, r1, slice=(0, 0, 2, 0, 0, 2, 4, 0, 4)),
+             Step("transfer", "H0", "M", hpt, mpt, r2, slice=(0, 0, 2, 0, 0, 2, 0, 0, 4)),
+             Step("transfer", "H1", "M", hpt, mpt, r2, slice=(0, 0, 2, 0, 0, 2, 0, 4, 4))]
+    wl = Workload("case", "tp split/merge", {"A": S, "H0": half, "H1": half, "M": S}, steps,
+                  value_seed=8, prefill_tag=8)
+    got, errs = check(wl)
+    assert errs == [0, 0, 0, 0]
+
+
+@pytest.mark.parametrize("src_pt,dst_pt,row,bits", [
+    ([0, 4], [0, 1], [0, 0, 0, 0, 0, 8], 1),
+    ([7, 1], [-1, 1], [0, 0, 0, 0, 0, 4], 2),
+    ([0], [0, 1], [0, 0, 0, 0, 0, 8], 4),
+    ([0, 1], [0, 1], [0, 0, 0, 0, 0, -2], 8),
+])
+def test_slice_device_errors(src_pt, dst_pt, row, bits):
+    S = PoolSpec(2, 2, 2, 8, T=4, N=4, e=2, layout="LPCTHD")
+    Dp = PoolSpec(1, 1, 2, 8, T=4, N=4, e=2, layout="LPCHTD")
+    wl = Workload("case", "slice errors", {"A": S, "B": Dp},
+                  [Step("transfer", "A", "B", np.asarray(src_pt, np.int32),
+                        np.asarray(dst_pt, np.int32), np.asarray([row], np.int64),
+                        slice=(1, 0, 1, 1, 0, 1, 0, 0, 2))], value_seed=2, prefill_tag=3)
+    _, errs = check(wl)
+    assert errs == [bits]
+
+
+# ---------------------------------------------------------------------------
 # error behaviour
 # ---------------------------------------------------------------------------
 

@@ -12,7 +12,8 @@ def _pages_needed(start, n, T):
 
 @pytest.mark.parametrize("k,small", [("tiny", False), ("handoff", False), ("relayout", False),
                                      ("mla", False), ("host_tier", False), ("handoff", True),
-                                     ("relayout", True), ("mla", True), ("host_tier", True)])
+                                     ("relayout", True), ("mla", True), ("host_tier", True),
+                                     ("tp_reshard", False), ("tp_reshard", True)])
 def test_tables_cover_and_destinations_are_disjoint(k, small):
     wl = W.get(k, small=small)
     for st in wl.steps:
