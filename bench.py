@@ -74,7 +74,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="handoff",
-                    choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard"])
+                    choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork"])
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="layers of the workload the CPU oracle runs (0: skip)")
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
@@ -154,6 +154,15 @@ def main() -> int:
         else:
             kvx.kvx_scatter(mem[st.src], S, mem[st.dst], D, d["dpt"], d["reqs"], errw)
 
+    # a copy inside one pool is checked against the pool as it was before
+    same_pool = len(wl.steps) == 1 and wl.steps[0].src == wl.steps[0].dst
+    before_layers = {}
+    if same_pool and args.cpu_layers > 0:
+        from oracle import layer_check
+        S0 = wl.sides[wl.steps[0].src]
+        for l in _layer_picks(S0.L, args.cpu_layers):
+            before_layers[l] = layer_check.pool_layer(mem[wl.steps[0].src], S0, l)
+
     log(f"warmup: {args.warmup} steps")
     for _ in range(args.warmup):
         for d in dsteps:
@@ -209,7 +218,7 @@ def main() -> int:
                     "kernel_ms": round(kern_ms[i_dom], 4)}
 
     context = {"kernel_sha": kernel_sha(), "per_step_kernel_ms": [round(x, 4) for x in kern_ms]}
-    if not args.no_memcpy and not host_leg:
+    if not args.no_memcpy and not host_leg and not same_pool:
         # hipMemcpyAsync D2D of the same byte count, as the achievable copy rate
         st = wl.steps[0]
         nb = min(dom_bytes // 2, mem[st.src].numel(), mem[st.dst].numel())
@@ -254,18 +263,16 @@ def main() -> int:
         from oracle import layer_check
         st = wl.steps[0]
         S, D = wl.sides[st.src], wl.sides[st.dst]
-        L = S.L
-        picks = sorted({round(i * (L - 1) / max(1, args.cpu_layers - 1))
-                        for i in range(min(args.cpu_layers, L))})
+        L = st.slice[2] if st.slice is not None else S.L
+        picks = _layer_picks(L, args.cpu_layers)
         secs, moved, exact = 0.0, 0, True
-        if st.slice is not None:
-            L = st.slice[2]
-            picks = sorted({round(i * (L - 1) / max(1, args.cpu_layers - 1))
-                            for i in range(min(args.cpu_layers, L))})
         for l in picks:
-            check = (layer_check.check_transfer_slice_layer if st.slice is not None
-                     else layer_check.check_transfer_layer)
-            r = check(mem[st.src], S, mem[st.dst], D, st, l, wl.prefill_tag)
+            if st.slice is not None:
+                r = layer_check.check_transfer_slice_layer(mem[st.src], S, mem[st.dst], D, st, l,
+                                                           wl.prefill_tag)
+            else:
+                r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l,
+                                                     wl.prefill_tag, before_layers.get(l))
             log(f"cpu oracle layer {l}: {r.oracle_seconds:.2f} s, bit-exact={r.equal}")
             secs += r.oracle_seconds
             moved += r.moved_bytes
@@ -298,6 +305,11 @@ def main() -> int:
     }
     print(json.dumps(out), flush=True)
     return 0
+
+
+def _layer_picks(L: int, k: int) -> list:
+    """k layers spread evenly over [0, L)."""
+    return sorted({round(i * (L - 1) / max(1, k - 1)) for i in range(min(k, L))})
 
 
 def _cpu_model() -> str:

@@ -52,8 +52,12 @@
  *     skipped.
  * - The destination side is resolved before the source side, so a
  *   position bad on both sides reports only the destination bit.
- * - Not detected: two records that write the same destination slot, and
- *   source and destination memory that overlap.  Both give undefined
+ * - Source and destination may be the same pool.  Copy-on-write of shared
+ *   pages (Sec. 4.1.4) copies pages into fresh pages of the same pool.  The
+ *   result is defined as long as no element the call writes is also read by
+ *   it.
+ * - Not detected: two records that write the same destination slot, and an
+ *   element that one call both reads and writes.  Both give undefined
  *   results.
  */
 #ifndef KVX_H

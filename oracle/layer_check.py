@@ -73,13 +73,20 @@ class LayerResult:
     moved_bytes: int      # algorithmic bytes (read + write) of this layer
 
 
-def check_transfer_layer(src_t, S, dst_t, D, step, l: int, tag: int) -> LayerResult:
+def check_transfer_layer(src_t, S, dst_t, D, step, l: int, tag: int,
+                         dst_before: np.ndarray | None = None) -> LayerResult:
     """Run the oracle on layer l of a pool -> pool step and compare it with
-    the device result."""
+    the device result.  The destination starts from its offset-coded
+    prefill, or from ``dst_before`` (host bytes of the layer before the
+    copy) when the step copies within one pool."""
     s1, d1 = one_layer(S), one_layer(D)
-    src = pool_layer(src_t, S, l)
     got = pool_layer(dst_t, D, l)
-    want = pool_layer_prefill(D, l, tag)
+    if dst_before is not None:
+        want = dst_before.copy()
+        src = dst_before if src_t is dst_t else pool_layer(src_t, S, l)
+    else:
+        want = pool_layer_prefill(D, l, tag)
+        src = pool_layer(src_t, S, l)
     t0 = time.perf_counter()
     err = kvx_oracle.default().transfer(src, s1, want, d1, step.src_pt, step.dst_pt, step.reqs)
     dt = time.perf_counter() - t0

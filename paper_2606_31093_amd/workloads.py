@@ -280,7 +280,34 @@ def tp_reshard(small: bool = False) -> Workload:
     return wl
 
 
-NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier", "tp_reshard")
+def cow_fork(small: bool = False) -> Workload:
+    """Copy-on-write inside one pool (Sec. 4.1.4): 16 requests of the handoff
+    shape are forked, each copied page by page into fresh pages of the same
+    pool (a fork duplicates shared pages before it appends).  Source and
+    destination pages are disjoint, drawn from one permutation of the pool."""
+    if small:
+        rng = np.random.default_rng(1107)
+        L, H, N, nreq, lo, hi = 3, 2, 64, 3, 1, 600
+    else:
+        rng = np.random.default_rng(1007)
+        L, H, N, nreq, lo, hi = 36, 8, 4096, 16, 1024, 8192
+    pool = PoolSpec(L, 2, H, 128, T=64, N=N, e=2, layout="LPCTHD")
+    lengths = [int(x) for x in rng.integers(lo, hi + 1, size=nreq)]
+    perm = rng.permutation(N).astype(np.int32)
+    counts = [_ceil_div(n, pool.T) for n in lengths]
+    total = sum(counts)
+    if 2 * total > N:
+        raise ValueError("pool too small for the fork")
+    src_pt, offs = _take_pages(perm[:total], counts)
+    dst_pt, _ = _take_pages(perm[total:2 * total], counts)
+    rows = [[o, o, 0, 0, 0, n] for o, n in zip(offs, lengths)]
+    step = Step("transfer", "A", "A", src_pt, dst_pt, _reqs(rows))
+    return Workload("cow_fork", f"copy-on-write fork {L}L x {H}H x 128, {nreq} requests "
+                    f"duplicated inside one 64-token pool", {"A": pool}, [step],
+                    value_seed=2007, prefill_tag=7, notes={"lengths": lengths})
+
+
+NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork")
 
 
 def get(name: str, small: bool = False) -> Workload:
@@ -288,7 +315,8 @@ def get(name: str, small: bool = False) -> Workload:
     if name == "tiny":
         return tiny()
     return {"handoff": handoff, "relayout": relayout, "mla": mla,
-            "host_tier": host_tier, "tp_reshard": tp_reshard}[name](small=small)
+            "host_tier": host_tier, "tp_reshard": tp_reshard,
+            "cow_fork": cow_fork}[name](small=small)
 
 
 def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:

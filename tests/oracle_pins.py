@@ -585,11 +585,42 @@ def pin_slice_errors(O):
             _same(d, base, "skipped positions written")
 
 
+
+# ---------------------------------------------------------------------------
+# copy-on-write inside one pool
+# ---------------------------------------------------------------------------
+
+def pin_same_pool_copy_on_write(O):
+    """Sec. 4.1.4: a request forks from a shared prefix whose last page is
+    partly filled; its copy of that page goes to a fresh page of the same
+    pool before it appends.  Source and destination are the same array; the
+    pages written are disjoint from the pages read, so the copy equals the
+    numpy statement (which reads everything before writing)."""
+    for layout in LAYOUTS:
+        P = PoolSpec(2, 2, 3, 8, T=8, N=12, e=2, layout=layout)
+        pool = _pool_bytes(P, 41)
+        # shared prefix: pages [5, 2, 9], 20 tokens (page 9 holds slots 0..3)
+        # fork A copies its partial last page 9 -> fresh page 7 (positions 16..19)
+        # fork B duplicates the whole prefix into fresh pages [0, 11, 3]
+        src_pt = np.array([5, 2, 9], np.int32)
+        dst_pt = np.array([0, 11, 3, 7], np.int32)
+        reqs = [_req(so=2, do=3, s0=0, d0=0, n=4),        # page 9 slots 0..3 -> page 7
+                _req(so=0, do=0, s0=0, d0=0, n=20)]       # prefix -> pages 0, 11, 3
+        want = pool.copy()
+        npr.transfer(pool.copy(), P, want, P, src_pt, dst_pt, reqs)
+        got = pool.copy()
+        assert O.transfer(got, P, got, P, src_pt, dst_pt, reqs) == 0
+        _same(got, want, f"copy-on-write {layout}")
+        V = npr.canon(got, P)
+        assert np.array_equal(V[:, 7, :, :4], V[:, 9, :, :4])            # forked page
+        assert np.array_equal(V[:, [0, 11], :, :], V[:, [5, 2], :, :])   # duplicated prefix
+
+
 PINS = [pin_hand_example, pin_hand_example_plchtd, pin_numpy_transfer,
         pin_numpy_transfer_widths, pin_numpy_gather_scatter, pin_identity_tables,
         pin_roundtrip, pin_bijection, pin_errors, pin_max_position, pin_tiny_workload,
         pin_slice_hand_example, pin_slice_numpy, pin_slice_decomposes_transfer,
-        pin_slice_tp_roundtrip, pin_slice_errors]
+        pin_slice_tp_roundtrip, pin_slice_errors, pin_same_pool_copy_on_write]
 
 
 def run_all(O) -> list:

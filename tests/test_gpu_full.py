@@ -54,26 +54,31 @@ def _free(torch, *objs):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("k", ["handoff", "relayout", "mla", "tp_reshard"])
+@pytest.mark.parametrize("k", ["handoff", "relayout", "mla", "tp_reshard", "cow_fork"])
 def test_full_transfer(torch, k):
     from oracle import layer_check
     wl, mem, dsteps = _setup(torch, k)
     st = dsteps[0]["st"]
     src = mem[st.src]
-    before = int(src.view(torch.int64).sum().item())
+    S, D = wl.sides[st.src], wl.sides[st.dst]
+    n_layers = st.slice[2] if st.slice is not None else S.L
+    layers = sorted({0, n_layers // 2, n_layers - 1})
+    same_pool = st.src == st.dst
+    # a copy inside one pool starts from the pool's values, not a prefill
+    dst_before = {l: layer_check.pool_layer(mem[st.dst], D, l) for l in layers} if same_pool else {}
+    before = int(src.view(torch.int64).sum().item()) if not same_pool else None
     print(f"{k}: {wl.title}", flush=True)
     for _ in range(2):                       # repeated launches write the same bytes
         assert _run(torch, wl, mem, dsteps[0]) == 0
-    assert int(src.view(torch.int64).sum().item()) == before, "source pool modified"
-    S, D = wl.sides[st.src], wl.sides[st.dst]
-    n_layers = st.slice[2] if st.slice is not None else S.L
-    for l in sorted({0, n_layers // 2, n_layers - 1}):
+    if not same_pool:
+        assert int(src.view(torch.int64).sum().item()) == before, "source pool modified"
+    for l in layers:
         if st.slice is not None:
             r = layer_check.check_transfer_slice_layer(mem[st.src], S, mem[st.dst], D, st, l,
                                                        wl.prefill_tag)
         else:
             r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l,
-                                                 wl.prefill_tag)
+                                                 wl.prefill_tag, dst_before.get(l))
         print(f"  layer {l}: oracle {r.oracle_seconds:.2f} s, equal={r.equal}", flush=True)
         assert r.equal, f"{k} layer {l} differs from the oracle"
     _free(torch, mem, dsteps)

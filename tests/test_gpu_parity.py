@@ -35,7 +35,8 @@ def test_tiny_workload():
     check(get("tiny"))
 
 
-@pytest.mark.parametrize("name", ["handoff", "relayout", "mla", "host_tier"])
+@pytest.mark.parametrize("name", ["handoff", "relayout", "mla", "host_tier", "tp_reshard",
+                                  "cow_fork"])
 def test_small_workloads(name):
     check(get(name, small=True))
 
@@ -130,6 +131,20 @@ def test_slice_device_errors(src_pt, dst_pt, row, bits):
                         slice=(1, 0, 1, 1, 0, 1, 0, 0, 2))], value_seed=2, prefill_tag=3)
     _, errs = check(wl)
     assert errs == [bits]
+
+
+@pytest.mark.parametrize("layout", ["LPCTHD", "LPCHTD", "PLCTHD", "PLCHTD"])
+def test_same_pool_copy_on_write(layout):
+    """A fork copies its partial last page, and another its whole prefix,
+    into fresh pages of the same pool (source and destination are one
+    allocation)."""
+    P = PoolSpec(2, 2, 3, 64, T=8, N=12, e=2, layout=layout)
+    rows = np.asarray([[2, 3, 0, 0, 0, 4], [0, 0, 0, 0, 0, 20], [0, 4, 0, 3, 0, 9]], np.int64)
+    wl = Workload("case", f"copy-on-write {layout}", {"A": P},
+                  [Step("transfer", "A", "A", np.asarray([5, 2, 9], np.int32),
+                        np.asarray([0, 11, 3, 7, 1, 4], np.int32), rows)],
+                  value_seed=41, prefill_tag=1)
+    check(wl)
 
 
 # ---------------------------------------------------------------------------

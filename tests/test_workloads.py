@@ -13,7 +13,8 @@ def _pages_needed(start, n, T):
 @pytest.mark.parametrize("k,small", [("tiny", False), ("handoff", False), ("relayout", False),
                                      ("mla", False), ("host_tier", False), ("handoff", True),
                                      ("relayout", True), ("mla", True), ("host_tier", True),
-                                     ("tp_reshard", False), ("tp_reshard", True)])
+                                     ("tp_reshard", False), ("tp_reshard", True),
+                                     ("cow_fork", False), ("cow_fork", True)])
 def test_tables_cover_and_destinations_are_disjoint(k, small):
     wl = W.get(k, small=small)
     for st in wl.steps:
