@@ -74,7 +74,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="handoff",
-                    choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork"])
+                    choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
+                             "handoff_layered"])
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="layers of the workload the CPU oracle runs (0: skip)")
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
@@ -137,14 +138,20 @@ def main() -> int:
             st=st,
             spt=kvx.device_table(st.src_pt, dev) if st.src_pt is not None else None,
             dpt=kvx.device_table(st.dst_pt, dev) if st.dst_pt is not None else None,
-            reqs=kvx.device_reqs(st.reqs, dev)))
+            reqs=kvx.device_reqs(st.reqs, dev),
+            events=[torch.cuda.Event(enable_timing=True)
+                    for _ in range(-(-wl.sides[st.src].L // st.layer_group))]
+            if st.layer_group else None))
     errw = torch.zeros(1, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
     def launch(d):
         st = d["st"]
         S, D = wl.sides[st.src], wl.sides[st.dst]
-        if st.op == "transfer" and st.slice is not None:
+        if st.op == "transfer" and st.layer_group:
+            kvx.kvx_transfer_layered(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
+                                     st.layer_group, d["events"], st.slice, errw)
+        elif st.op == "transfer" and st.slice is not None:
             kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["spt"], d["dpt"],
                                    d["reqs"], errw)
         elif st.op == "transfer":
@@ -218,6 +225,12 @@ def main() -> int:
                     "kernel_ms": round(kern_ms[i_dom], 4)}
 
     context = {"kernel_sha": kernel_sha(), "per_step_kernel_ms": [round(x, 4) for x in kern_ms]}
+    for i, d in enumerate(dsteps):
+        if d["events"]:
+            # completion time of each layer group, from the start of the last timed step
+            e_start = events[i][-1][0]
+            context["layer_group_done_ms"] = [round(e_start.elapsed_time(ev), 4)
+                                              for ev in d["events"]]
     if not args.no_memcpy and not host_leg and not same_pool:
         # hipMemcpyAsync D2D of the same byte count, as the achievable copy rate
         st = wl.steps[0]

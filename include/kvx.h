@@ -183,6 +183,27 @@ int kvx_transfer_slice(const kvx_pool *src, const kvx_pool *dst, const kvx_slice
                        const kvx_req *reqs, int32_t n_reqs,
                        uint32_t *dev_err, void *stream);
 
+/* Layer-pipelined pool -> pool transfer (Sec. 7: hierarchical transmission;
+ * Sec. 5.1: pipelined prefill).  The copied layers (all of them when `slice`
+ * is NULL, else the slice's layer range) are moved in consecutive groups of
+ * layers_per_group layers, one launch per group, in order, on `stream`.
+ * After group g the call records events[g] on `stream`.  A consumer stream
+ * that waits on events[g] may use those layers of the destination while
+ * later groups are still moving.
+ * - events: hipEvent_t handles created by the caller (the library creates
+ *   none); n_events must be >= the number of groups.
+ * - Every event is recorded even when nothing is copied.  If a launch
+ *   fails, the call returns KVX_ERR_HIP, and the events of that group and
+ *   later groups are not recorded.
+ * - The data result equals kvx_transfer_slice / kvx_transfer with the same
+ *   arguments. */
+int kvx_transfer_layered(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                         const int32_t *src_pt, int64_t src_pt_len,
+                         const int32_t *dst_pt, int64_t dst_pt_len,
+                         const kvx_req *reqs, int32_t n_reqs,
+                         int32_t layers_per_group, void *const *events, int32_t n_events,
+                         uint32_t *dev_err, void *stream);
+
 /* Pool -> flat buffer: the offload (serialization) direction of Sec. 4.1.2. */
 int kvx_gather(const kvx_pool *src, const kvx_buf *dst,
                const int32_t *src_pt, int64_t src_pt_len,

@@ -6,6 +6,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <algorithm>
 #include <string>
 
 #include "kvx.h"
@@ -283,12 +284,14 @@ int check_slice(const kvx_slice &sl, const Shape &s, const Shape &d) {
     return KVX_OK;
 }
 
-// Pool -> pool; slice == NULL copies everything between equal shapes.
+// Pool -> pool; slice == NULL copies everything between equal shapes.  With
+// group > 0 the layer range is moved in groups of `group` layers, one launch
+// each, and events[g] is recorded on the stream after group g.
 int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
                   const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
                   int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err,
-                  void *stream) {
-    g_last_error.clear();
+                  void *stream, int32_t group = 0, void *const *events = nullptr,
+                  int32_t n_events = 0) {
     Shape ss, ds;
     int st;
     if ((st = check_pool(src, "src", ss))) return st;
@@ -304,18 +307,43 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
     if ((st = check_common(reqs, n_reqs, dev_err))) return st;
     if ((st = check_table(src_pt, src_pt_len, "src_pt"))) return st;
     if ((st = check_table(dst_pt, dst_pt_len, "dst_pt"))) return st;
-    if (n_reqs == 0 || sl.num_layers == 0 || sl.num_kv == 0 || sl.num_heads == 0) return KVX_OK;
+    int32_t groups = 1;
+    if (group > 0) {
+        groups = sl.num_layers == 0 ? 0 : (sl.num_layers + group - 1) / group;
+        if (n_events < groups)
+            return fail(KVX_ERR_RANGE, "%d layer groups need %d events, got %d", groups, groups,
+                        n_events);
+        if (groups > 0 && !events) return fail(KVX_ERR_NULL, "events is NULL");
+        for (int32_t g = 0; g < groups; ++g)
+            if (!events[g]) return fail(KVX_ERR_NULL, "events[%d] is NULL", g);
+    }
+    const bool empty = n_reqs == 0 || sl.num_layers == 0 || sl.num_kv == 0 || sl.num_heads == 0;
     Views v;
-    if ((st = view_all(src->base, dst->base, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, dev_err, v)))
+    if (!empty && (st = view_all(src->base, dst->base, src_pt, src_pt_len, dst_pt, dst_pt_len,
+                                 reqs, dev_err, v)))
         return st;
-    kvx::Params P{};
-    P.op = kvx::OP_TRANSFER;
-    P.src = pool_side(src, v.src, v.src_pt, src_pt_len, sl.src_layer0, sl.src_kv0, sl.src_head0,
-                      sl.num_heads);
-    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, sl.dst_layer0, sl.dst_kv0, sl.dst_head0,
-                      sl.num_heads);
-    finish_params(P, Shape{sl.num_layers, sl.num_kv, sl.num_heads, ss.D, ss.e}, v, n_reqs);
-    return enqueue(P, stream);
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    for (int32_t g = 0; g < groups; ++g) {
+        if (!empty) {
+            const int32_t l0 = group > 0 ? g * group : 0;
+            const int32_t nl = group > 0 ? std::min(group, sl.num_layers - l0) : sl.num_layers;
+            kvx::Params P{};
+            P.op = kvx::OP_TRANSFER;
+            P.src = pool_side(src, v.src, v.src_pt, src_pt_len, sl.src_layer0 + l0, sl.src_kv0,
+                              sl.src_head0, sl.num_heads);
+            P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, sl.dst_layer0 + l0, sl.dst_kv0,
+                              sl.dst_head0, sl.num_heads);
+            finish_params(P, Shape{nl, sl.num_kv, sl.num_heads, ss.D, ss.e}, v, n_reqs);
+            if ((st = enqueue(P, stream))) return st;
+        }
+        if (group > 0) {
+            const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(events[g]), hs);
+            if (e != hipSuccess)
+                return fail(KVX_ERR_HIP, "recording the event of layer group %d failed: %s", g,
+                            hipGetErrorString(e));
+        }
+    }
+    return KVX_OK;
 }
 
 }  // namespace
@@ -325,6 +353,7 @@ extern "C" {
 int kvx_transfer(const kvx_pool *src, const kvx_pool *dst, const int32_t *src_pt, int64_t src_pt_len,
                  const int32_t *dst_pt, int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs,
                  uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
     return transfer_impl(src, dst, nullptr, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
                          dev_err, stream);
 }
@@ -381,6 +410,18 @@ int kvx_scatter(const kvx_buf *src, const kvx_pool *dst, const int32_t *dst_pt, 
     P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, 0, 0, 0, ds.H);
     finish_params(P, ss, v, n_reqs);
     return enqueue(P, stream);
+}
+
+int kvx_transfer_layered(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                         const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
+                         int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs,
+                         int32_t layers_per_group, void *const *events, int32_t n_events,
+                         uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    if (layers_per_group < 1)
+        return fail(KVX_ERR_RANGE, "layers_per_group must be >= 1 (got %d)", layers_per_group);
+    return transfer_impl(src, dst, slice, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
+                         dev_err, stream, layers_per_group, events, n_events);
 }
 
 int64_t kvx_pool_bytes(const kvx_pool *pool) {

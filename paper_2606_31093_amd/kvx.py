@@ -4,7 +4,7 @@ Every step of the copy runs in the library's HIP kernels.  PyTorch supplies
 device memory and the stream: tensors are passed as raw pointers and the
 kernels run on ``torch.cuda.current_stream()`` unless a stream is given.
 The functions keep the C names: ``kvx_transfer``, ``kvx_transfer_slice``,
-``kvx_gather`` and ``kvx_scatter``.  A missing or unloadable library raises; there is no
+``kvx_transfer_layered``, ``kvx_gather`` and ``kvx_scatter``.  A missing or unloadable library raises; there is no
 fallback path.
 
 Pool and buffer shapes are duck-typed: a pool shape has integer attributes
@@ -96,9 +96,12 @@ def lib() -> ctypes.CDLL:
         L.kvx_transfer.argtypes = [pp, pp, vp, i64, vp, i64, vp, i32, vp, vp]
         L.kvx_transfer_slice.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp, i32,
                                          vp, vp]
+        L.kvx_transfer_layered.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp,
+                                           i32, i32, ctypes.POINTER(vp), i32, vp, vp]
         L.kvx_gather.argtypes = [pp, bp, vp, i64, vp, i32, vp, vp]
         L.kvx_scatter.argtypes = [bp, pp, vp, i64, vp, i32, vp, vp]
-        for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_gather, L.kvx_scatter):
+        for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_transfer_layered, L.kvx_gather,
+                  L.kvx_scatter):
             f.restype = ctypes.c_int
         L.kvx_pool_bytes.argtypes = [pp]
         L.kvx_pool_bytes.restype = ctypes.c_int64
@@ -234,6 +237,33 @@ def kvx_transfer_slice(src, src_spec, dst, dst_spec, sl, src_pt, dst_pt, reqs, d
     _check(lib().kvx_transfer_slice(ctypes.byref(S), ctypes.byref(D), ctypes.byref(X),
                                     _ptr(src_pt), _len(src_pt), _ptr(dst_pt), _len(dst_pt),
                                     _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
+
+
+def kvx_transfer_layered(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, layers_per_group,
+                         events, sl=None, dev_err=None, stream=None) -> None:
+    """Layer-pipelined pool -> pool (see kvx_transfer_layered in
+    include/kvx.h).  ``events`` are ``torch.cuda.Event`` objects (or raw
+    hipEvent_t handles), one per layer group; the library records events[g]
+    on the stream once group g has been copied."""
+    import torch
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    st = _stream(stream)
+    handles = []
+    for ev in events:
+        if isinstance(ev, int):
+            handles.append(ev)
+            continue
+        if not ev.cuda_event:          # torch creates the HIP event on first record
+            ev.record(torch.cuda.ExternalStream(st) if stream is not None else None)
+        handles.append(ev.cuda_event)
+    arr = (ctypes.c_void_p * max(1, len(handles)))(*handles)
+    S, D = pool_desc(src_spec, src), pool_desc(dst_spec, dst)
+    X = None if sl is None else ctypes.byref(slice_desc(sl))
+    _check(lib().kvx_transfer_layered(ctypes.byref(S), ctypes.byref(D), X, _ptr(src_pt),
+                                      _len(src_pt), _ptr(dst_pt), _len(dst_pt), _ptr(reqs),
+                                      _n_reqs(reqs), int(layers_per_group), arr, len(handles),
+                                      _ptr(dev_err), st))
 
 
 def kvx_gather(src, src_spec, dst, buf_spec, src_pt, reqs, dev_err=None, stream=None) -> None:

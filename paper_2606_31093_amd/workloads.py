@@ -91,6 +91,7 @@ class Step:
     dst_pt: np.ndarray | None    # int32 page table of a pool destination
     reqs: np.ndarray             # (n, 6) int64 request records
     slice: tuple | None = None   # transfer of a layer/kv/head range: nine fields
+    layer_group: int = 0         # > 0: layer-pipelined, this many layers per group
 
     @property
     def n_tokens(self) -> int:
@@ -307,7 +308,19 @@ def cow_fork(small: bool = False) -> Workload:
                     value_seed=2007, prefill_tag=7, notes={"lengths": lengths})
 
 
-NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork")
+def handoff_layered(small: bool = False) -> Workload:
+    """The handoff moved in groups of 4 layers, with a completion event per
+    group, so a consumer can start on early layers while later ones move
+    (Sec. 7: hierarchical transmission; Sec. 5.1: pipelined prefill)."""
+    wl = handoff(small)
+    wl.name = "handoff_layered"
+    wl.title = wl.title + ", in 4-layer groups"
+    wl.steps[0].layer_group = 1 if small else 4
+    return wl
+
+
+NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
+         "handoff_layered")
 
 
 def get(name: str, small: bool = False) -> Workload:
@@ -316,7 +329,7 @@ def get(name: str, small: bool = False) -> Workload:
         return tiny()
     return {"handoff": handoff, "relayout": relayout, "mla": mla,
             "host_tier": host_tier, "tp_reshard": tp_reshard,
-            "cow_fork": cow_fork}[name](small=small)
+            "cow_fork": cow_fork, "handoff_layered": handoff_layered}[name](small=small)
 
 
 def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:

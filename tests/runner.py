@@ -70,7 +70,12 @@ def run_gpu(wl, init: dict, raw_reqs=None) -> tuple[dict, list]:
         S, D = wl.sides[st.src], wl.sides[st.dst]
         spt = kvx.device_table(st.src_pt, dev) if st.src_pt is not None else None
         dpt = kvx.device_table(st.dst_pt, dev) if st.dst_pt is not None else None
-        if st.op == "transfer" and st.slice is not None:
+        if st.op == "transfer" and st.layer_group:
+            n_layers = st.slice[2] if st.slice is not None else S.L
+            events = [torch.cuda.Event() for _ in range(-(-n_layers // st.layer_group))]
+            kvx.kvx_transfer_layered(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs,
+                                     st.layer_group, events, st.slice, err)
+        elif st.op == "transfer" and st.slice is not None:
             kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, spt, dpt, reqs, err)
         elif st.op == "transfer":
             kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs, err)

@@ -205,6 +205,21 @@ def test_slice_host_validation(lib, S, D, sl, n_reqs, status):
     assert _call_slice(S, D, sl, n_reqs) == status
 
 
+def test_layered_host_validation(lib):
+    L = kvx.lib()
+    sp, dp = kvx.pool_desc(BIG, FAKE), kvx.pool_desc(BIG, FAKE)
+    ev = (ctypes.c_void_p * 4)(FAKE, FAKE, FAKE, None)
+
+    def call(group, events, n_events, n_reqs=1):
+        return L.kvx_transfer_layered(ctypes.byref(sp), ctypes.byref(dp), None, FAKE, 1, FAKE, 1,
+                                      FAKE, n_reqs, group, events, n_events, None, None)
+    assert call(0, ev, 4) == -5                 # group size must be >= 1
+    assert call(1, ev, 3) == -5                 # 4 layers need 4 events
+    assert call(2, None, 2) == -1               # no event array
+    assert call(1, ev, 4) == -1                 # events[3] is NULL
+    assert "events[3]" in kvx.kvx_last_error()
+
+
 def test_slice_reserved_must_be_zero(lib):
     x = kvx.slice_desc((0, 0, 1, 0, 0, 1, 0, 0, 1))
     x.reserved = 3

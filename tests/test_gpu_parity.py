@@ -36,7 +36,7 @@ def test_tiny_workload():
 
 
 @pytest.mark.parametrize("name", ["handoff", "relayout", "mla", "host_tier", "tp_reshard",
-                                  "cow_fork"])
+                                  "cow_fork", "handoff_layered"])
 def test_small_workloads(name):
     check(get(name, small=True))
 
@@ -145,6 +145,68 @@ def test_same_pool_copy_on_write(layout):
                         np.asarray([0, 11, 3, 7, 1, 4], np.int32), rows)],
                   value_seed=41, prefill_tag=1)
     check(wl)
+
+
+# ---------------------------------------------------------------------------
+# layer-pipelined transfer
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("group", [1, 2, 3, 5])
+@pytest.mark.parametrize("with_slice", [False, True])
+def test_layered_matches_oracle(group, with_slice):
+    if with_slice:
+        wl = cases.slice_case("LPCTHD", "PLCHTD", 4, 8, (5, 2, 4), (4, 2, 2),
+                              (1, 0, 4, 0, 0, 2, 2, 0, 2), seed=group)
+    else:
+        wl = cases.transfer_case("LPCHTD", "LPCTHD", 16, 32, seed=group, L=5)
+    wl.steps[0].layer_group = group
+    check(wl)
+
+
+def test_layered_events_guard_consumers():
+    """A consumer stream waits on each group's event, then snapshots that
+    group's destination layers; every snapshot matches the oracle."""
+    import torch
+    from paper_2606_31093_amd import kvx
+    from oracle import kvx_oracle
+    wl = get("handoff", small=True)
+    st = wl.steps[0]
+    S = wl.sides["A"]
+    S6 = PoolSpec(6, S.C, S.H, S.D, S.T, S.N, S.e, S.layout)
+    init = initial_bytes(Workload("case", "", {"A": S6, "B": S6}, [st], 5, 5))
+    want = init["B"].copy()
+    assert kvx_oracle.default().transfer(init["A"], S6, want, S6, st.src_pt, st.dst_pt,
+                                         st.reqs) == 0
+    a = torch.from_numpy(init["A"]).cuda()
+    b = torch.from_numpy(init["B"]).cuda()
+    per_layer = S6.nbytes // S6.L
+    events = [torch.cuda.Event() for _ in range(3)]
+    producer, consumer = torch.cuda.Stream(), torch.cuda.Stream()
+    snaps = []
+    with torch.cuda.stream(producer):
+        kvx.kvx_transfer_layered(a, S6, b, S6, kvx.device_table(st.src_pt),
+                                 kvx.device_table(st.dst_pt), kvx.device_reqs(st.reqs), 2, events,
+                                 stream=producer)
+    for g in range(3):
+        consumer.wait_event(events[g])
+        with torch.cuda.stream(consumer):
+            snaps.append(b[2 * g * per_layer:(2 * g + 2) * per_layer].clone())
+    torch.cuda.synchronize()
+    for g, snap in enumerate(snaps):
+        assert np.array_equal(snap.cpu().numpy(),
+                              want[2 * g * per_layer:(2 * g + 2) * per_layer]), f"group {g}"
+
+
+def test_layered_records_events_when_empty():
+    import torch
+    from paper_2606_31093_amd import kvx
+    S = PoolSpec(3, 2, 1, 8, T=4, N=4, e=2, layout="LPCTHD")
+    a = torch.zeros(S.nbytes, dtype=torch.uint8, device="cuda")
+    events = [torch.cuda.Event() for _ in range(3)]
+    empty = torch.empty(0, dtype=torch.uint8, device="cuda")
+    kvx.kvx_transfer_layered(a, S, a.clone(), S, None, None, empty, 1, events)
+    torch.cuda.synchronize()
+    assert all(ev.query() for ev in events)
 
 
 # ---------------------------------------------------------------------------
