@@ -38,9 +38,10 @@ if ROOT not in sys.path:
 METRIC = "KV transfer GB/s (read+write) and % of HBM/host-link peak, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, published
 PCIE_PEAK_GBPS = 63.0         # PCIe 5.0 x16 per direction: 32 GT/s x 16 x 128/130 / 8
+# The copy kernel and its launch shape; a change here invalidates the
+# committed HBM counter records.
 KERNEL_SOURCES = ["paper_2606_31093_amd/csrc/kvx_kernels.hip",
-                  "paper_2606_31093_amd/csrc/kvx_internal.h",
-                  "paper_2606_31093_amd/csrc/kvx_api.cpp", "include/kvx.h"]
+                  "paper_2606_31093_amd/csrc/kvx_internal.h"]
 
 
 def log(msg: str) -> None:

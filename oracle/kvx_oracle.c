@@ -296,3 +296,73 @@ uint32_t ora_transfer_slice(const uint8_t *src, const ora_pool *S, uint8_t *dst,
     }
     return err;
 }
+
+/* ------------------------------------------------------------------------
+ * Chained page hashes (Sec. 5.1 "Chained Paged Hashing": each page's hash
+ * encodes the hash of its predecessor, so two hashes are equal only when the
+ * whole prefix matches page by page).  The paper names no hash function;
+ * this build's definition:
+ *
+ *   fnv(bytes, h): FNV-1a 64 (Fowler, Noll and Vo): for each byte b in
+ *       order, h = (h xor b) * 0x100000001b3 mod 2^64; the empty-input state
+ *       is the offset basis 0xcbf29ce484222325.
+ *   Request r covers positions [off_r, off_r + n_r) of a payload of records
+ *   of rec_bytes bytes (token ids, modality digests).  Page j holds its
+ *   positions [j*T, min((j+1)*T, n_r)).
+ *   c_j = fnv(bytes of page j, basis)                 (page digest)
+ *   h_j = fnv(le64(h_{j-1}) || le64(c_j), basis)      (chain), h_{-1} = seed_r
+ *   out[out_off_r + j] = h_j for j < ceil(n_r / T).
+ *
+ * A request continues an earlier chain by passing the hash of its last
+ * full page as seed (incremental matching, Sec. 5.1).  A malformed record
+ * (n < 0, positions or outputs outside the arrays) is skipped and raises
+ * ORA_ERR_BAD_REQ.  Hash records are rows of four int64 values:
+ *   payload_off (positions), out_off, seed (bits), n_positions.
+ * ------------------------------------------------------------------------ */
+#define FNV_BASIS 0xcbf29ce484222325ull
+#define FNV_PRIME 0x100000001b3ull
+
+uint64_t ora_fnv1a64(const uint8_t *p, int64_t n, uint64_t h)
+{
+    for (int64_t i = 0; i < n; ++i) {
+        h ^= p[i];
+        h *= FNV_PRIME;
+    }
+    return h;
+}
+
+static void le64(uint8_t *out, uint64_t v)
+{
+    for (int b = 0; b < 8; ++b)
+        out[b] = (uint8_t)(v >> (8 * b));
+}
+
+uint32_t ora_page_hashes(const uint8_t *payload, int64_t payload_positions,
+                         int64_t rec_bytes, int64_t T, const int64_t *reqs,
+                         int64_t n_reqs, uint64_t *out, int64_t out_len)
+{
+    uint32_t err = 0;
+    for (int64_t r = 0; r < n_reqs; ++r) {
+        const int64_t *q = reqs + 4 * r;
+        int64_t off = q[0], out_off = q[1], n = q[3];
+        uint64_t h = (uint64_t)q[2];
+        int64_t pages = n > 0 ? (n + T - 1) / T : 0;
+        if (n < 0 || off < 0 || off + n > payload_positions || out_off < 0 ||
+            out_off + pages > out_len) {
+            err |= ORA_ERR_BAD_REQ;
+            continue;
+        }
+        for (int64_t j = 0; j < pages; ++j) {
+            int64_t first = j * T;
+            int64_t count = (n - first < T) ? n - first : T;
+            uint64_t c = ora_fnv1a64(payload + (off + first) * rec_bytes,
+                                     count * rec_bytes, FNV_BASIS);
+            uint8_t pair[16];
+            le64(pair, h);
+            le64(pair + 8, c);
+            h = ora_fnv1a64(pair, 16, FNV_BASIS);
+            out[out_off + j] = h;
+        }
+    }
+    return err;
+}

@@ -10,7 +10,8 @@ compiles it with gcc, loads it with ctypes and marshals numpy arrays.  What it
 computes is stated in the C file's header: Omni-Flow Sec. 4.1.1 (layer x page
 x slice addressing), Sec. 4.1.2 (conversion between the paged layout and the
 flat serialization), Sec. 4.1.4 (partial pages keep their other slots) and
-Sec. 5.2 (slot-to-page translation through a page table).
+Sec. 5.2 (slot-to-page translation through a page table); and the chained
+page hashes of Sec. 5.1 (FNV-1a 64 page digests chained page by page).
 
 Inputs are duck-typed: a pool shape is any object with integer attributes
 ``L C H D T N e`` and a ``layout`` name (``"LPCTHD"``, ``"LPCHTD"``,
@@ -118,6 +119,10 @@ class Oracle:
         lib.ora_scatter.restype = u32
         lib.ora_transfer_slice.argtypes = [vp, pp, vp, pp, vp, vp, i64, vp, i64, vp, i64]
         lib.ora_transfer_slice.restype = u32
+        lib.ora_fnv1a64.argtypes = [vp, i64, ctypes.c_uint64]
+        lib.ora_fnv1a64.restype = ctypes.c_uint64
+        lib.ora_page_hashes.argtypes = [vp, i64, i64, i64, vp, i64, vp, i64]
+        lib.ora_page_hashes.restype = u32
         self.lib = lib
 
     def transfer(self, src: np.ndarray, src_shape, dst: np.ndarray, dst_shape,
@@ -187,6 +192,29 @@ class Oracle:
             _ptr(sp), np.asarray(src_pt).size, _ptr(dp), np.asarray(dst_pt).size,
             _ptr(rq), nr))
 
+    def fnv1a64(self, data: bytes, h: int = 0xcbf29ce484222325) -> int:
+        """FNV-1a 64 of ``data`` continued from state ``h``."""
+        buf = np.frombuffer(bytes(data), dtype=np.uint8) if data else np.zeros(1, np.uint8)
+        return int(self.lib.ora_fnv1a64(_ptr(buf), len(data), h))
+
+    def page_hashes(self, payload: np.ndarray, rec_bytes: int, T: int, hreqs, out: np.ndarray) -> int:
+        """Chained page hashes (see ora_page_hashes).  ``payload`` holds
+        records of ``rec_bytes`` bytes; ``hreqs`` rows are (payload_off,
+        out_off, seed, n_positions); ``out`` (uint64) is updated in place."""
+        if payload.nbytes % rec_bytes:
+            raise ValueError("payload is not a whole number of records")
+        p = np.ascontiguousarray(payload).view(np.uint8).reshape(-1)
+        if out.dtype != np.uint64 or not out.flags.c_contiguous:
+            raise TypeError("out must be a contiguous uint64 array")
+        rows = np.ascontiguousarray(
+            np.asarray([[int(a), int(b), int(c) - (1 << 64) if int(c) >= 1 << 63 else int(c), int(d)]
+                        for a, b, c, d in hreqs], dtype=np.int64).reshape(-1, 4))
+        rq = rows if len(rows) else np.zeros((1, 4), np.int64)
+        return int(self.lib.ora_page_hashes(_ptr(p if p.size else np.zeros(1, np.uint8)),
+                                            p.size // rec_bytes, rec_bytes, T, _ptr(rq), len(rows),
+                                            _ptr(out if out.size else np.zeros(1, np.uint64)),
+                                            out.size))
+
 
 _DEFAULT: Oracle | None = None
 
@@ -215,3 +243,7 @@ def scatter(*a, **k) -> int:
 
 def transfer_slice(*a, **k) -> int:
     return default().transfer_slice(*a, **k)
+
+
+def page_hashes(*a, **k) -> int:
+    return default().page_hashes(*a, **k)

@@ -616,11 +616,101 @@ def pin_same_pool_copy_on_write(O):
         assert np.array_equal(V[:, [0, 11], :, :], V[:, [5, 2], :, :])   # duplicated prefix
 
 
+
+# ---------------------------------------------------------------------------
+# chained page hashes
+# ---------------------------------------------------------------------------
+
+FNV_BASIS = 0xcbf29ce484222325
+
+
+def pin_fnv_published_vectors(O):
+    """FNV-1a 64 test vectors published with the algorithm."""
+    for data, want in ((b"", 0xcbf29ce484222325), (b"a", 0xaf63dc4c8601ec8c),
+                       (b"foobar", 0x85944171f73967e8)):
+        assert O.fnv1a64(data) == want, (data, hex(O.fnv1a64(data)))
+
+
+def _hashes(O, payload, rec_bytes, T, rows, n_out):
+    out = np.zeros(n_out, np.uint64)
+    err = O.page_hashes(payload, rec_bytes, T, rows, out)
+    return err, [int(x) for x in out]
+
+
+def pin_hash_definition(O):
+    """A one-page request: its hash is the FNV-1a of the seed's and the page
+    digest's little-endian bytes, the digest being the FNV-1a of the page."""
+    rng = np.random.default_rng(3)
+    page = rng.integers(0, 2**31, size=16, dtype=np.int32)
+    for seed in (0, 0x0123456789ABCDEF, 2**64 - 1):
+        err, out = _hashes(O, page, 4, 16, [(0, 0, seed, 16)], 1)
+        c = O.fnv1a64(page.tobytes())
+        want = O.fnv1a64(seed.to_bytes(8, "little") + c.to_bytes(8, "little"))
+        assert err == 0 and out[0] == want
+
+
+def pin_hash_prefix_property(O):
+    """Requests that share their first k pages share their first k hashes
+    and differ from page k on (a changed page changes every later hash)."""
+    rng = np.random.default_rng(5)
+    T, n = 8, 70
+    a = rng.integers(0, 50000, size=n, dtype=np.int32)
+    b = a.copy()
+    b[3 * T + 2] += 1                      # page 3 differs
+    payload = np.concatenate([a, b, a])
+    rows = [(0, 0, 7, n), (n, 9, 7, n), (2 * n, 18, 7, n)]
+    err, out = _hashes(O, payload, 4, T, rows, 27)
+    assert err == 0
+    ha, hb, hc = out[0:9], out[9:18], out[18:27]
+    assert ha == hc
+    assert ha[:3] == hb[:3] and all(x != y for x, y in zip(ha[3:], hb[3:]))
+    assert len(set(ha)) == 9               # no two pages of a chain collide here
+
+
+def pin_hash_continuation(O):
+    """Hashing [0, n) equals hashing [0, kT) and then [kT, n) seeded with
+    the hash of page k - 1 (incremental matching)."""
+    rng = np.random.default_rng(6)
+    T, n, k = 4, 23, 3
+    pay = rng.integers(0, 2**31, size=n * 2, dtype=np.int32)     # 8-byte records
+    err, whole = _hashes(O, pay, 8, T, [(0, 0, 11, n)], 6)
+    err2, head = _hashes(O, pay, 8, T, [(0, 0, 11, k * T)], 3)
+    err3, tail = _hashes(O, pay, 8, T, [(k * T, 0, head[-1], n - k * T)], 3)
+    assert err == err2 == err3 == 0
+    assert whole == head + tail
+
+
+def pin_hash_partial_last_page(O):
+    """Positions past the end of a request are not part of its last page:
+    growing the request inside its last page changes that page's hash only."""
+    rng = np.random.default_rng(8)
+    pay = rng.integers(0, 2**31, size=32, dtype=np.int32)
+    _, short = _hashes(O, pay, 4, 8, [(0, 0, 0, 19)], 3)
+    _, longer = _hashes(O, pay, 4, 8, [(0, 0, 0, 21)], 3)
+    assert short[:2] == longer[:2] and short[2] != longer[2]
+    # and the partial page's digest covers only its 3 positions
+    c = O.fnv1a64(pay[16:19].tobytes())
+    assert short[2] == O.fnv1a64(short[1].to_bytes(8, "little") + c.to_bytes(8, "little"))
+
+
+def pin_hash_errors(O):
+    pay = np.arange(40, dtype=np.int32)
+    for row, bits in (((0, 0, 0, 40), 0), ((0, 0, 0, 41), ERR_BAD_REQ), ((-1, 0, 0, 4), ERR_BAD_REQ),
+                      ((0, 4, 0, 40), ERR_BAD_REQ), ((0, -1, 0, 4), ERR_BAD_REQ),
+                      ((0, 0, 0, -1), ERR_BAD_REQ), ((5, 0, 0, 0), 0)):
+        out = np.full(5, 77, np.uint64)
+        assert O.page_hashes(pay, 4, 10, [row], out) == bits, row
+        if bits:
+            assert (out == 77).all()
+
+
 PINS = [pin_hand_example, pin_hand_example_plchtd, pin_numpy_transfer,
         pin_numpy_transfer_widths, pin_numpy_gather_scatter, pin_identity_tables,
         pin_roundtrip, pin_bijection, pin_errors, pin_max_position, pin_tiny_workload,
         pin_slice_hand_example, pin_slice_numpy, pin_slice_decomposes_transfer,
-        pin_slice_tp_roundtrip, pin_slice_errors, pin_same_pool_copy_on_write]
+        pin_slice_tp_roundtrip, pin_slice_errors, pin_same_pool_copy_on_write,
+        pin_fnv_published_vectors, pin_hash_definition, pin_hash_prefix_property,
+        pin_hash_continuation, pin_hash_partial_last_page, pin_hash_errors]
 
 
 def run_all(O) -> list:

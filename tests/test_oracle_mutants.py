@@ -82,6 +82,15 @@ MUTANTS = {
     "slice_src_kv_offset_dropped": ("sl[3] + c", "c"),
     "slice_one_layer_short": ("l < sl[2]", "l + 1 < sl[2]"),
     "slice_heads_of_the_pool": ("h < sl[8]", "h < S->H"),
+    "fnv1_instead_of_fnv1a": ("        h ^= p[i];\n        h *= FNV_PRIME;",
+                              "        h *= FNV_PRIME;\n        h ^= p[i];"),
+    "chain_pair_swapped": ("le64(pair, h);\n            le64(pair + 8, c);",
+                           "le64(pair, c);\n            le64(pair + 8, h);"),
+    "digest_continues_chain": ("count * rec_bytes, FNV_BASIS);", "count * rec_bytes, h);"),
+    "seed_ignored": ("uint64_t h = (uint64_t)q[2];", "uint64_t h = 0;"),
+    "last_page_padded": ("int64_t count = (n - first < T) ? n - first : T;", "int64_t count = T;"),
+    "hash_out_shifted": ("out[out_off + j] = h;", "out[out_off + pages - 1 - j] = h;"),
+    "hash_bounds_unchecked": ("off + n > payload_positions ||", "0 ||"),
 }
 # Sites that occur in both the pool -> pool and the slice copy: mutate one
 # occurrence at a time (0: ora_transfer, 1: ora_transfer_slice).
