@@ -76,7 +76,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="handoff",
                     choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
-                             "handoff_layered"])
+                             "handoff_layered", "page_hash"])
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="layers of the workload the CPU oracle runs (0: skip)")
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
@@ -121,6 +121,8 @@ def main() -> int:
         log("libkvx.so missing: building")
         build_lib.build()
     kvx.lib()
+    if args.workload == "page_hash":
+        return hash_bench(args)
 
     dev = torch.device("cuda", 0)
     wl = workloads.get(args.workload)
@@ -318,6 +320,86 @@ def main() -> int:
         "context": context,
     }
     print(json.dumps(out), flush=True)
+    return 0
+
+
+# Valu instruction cost of one payload byte in the page-digest loop of the
+# hash kernel (gfx950 assembly): one quarter-rate 64-bit multiply-add, one
+# quarter-rate 32-bit multiply and three full-rate operations, i.e. 11 SIMD
+# cycles per byte per lane.  Peak: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz
+# / 11 cycles per byte.
+HASH_CYCLES_PER_BYTE = 11
+HASH_PEAK_GBPS = 256 * 4 * 16 * 2.4e9 / HASH_CYCLES_PER_BYTE / 1e9
+
+
+def hash_bench(args) -> int:
+    """Chained page hashes over token ids: GB/s of payload hashed."""
+    import numpy as np
+    import torch
+
+    from paper_2606_31093_amd import kvx, workloads
+    wl = workloads.page_hash()
+    log(f"workload: {wl.title}")
+    pay_np = workloads.hash_payload(wl)
+    dev = torch.device("cuda", 0)
+    pay = torch.from_numpy(pay_np.view(np.uint8).copy()).to(dev)
+    reqs = kvx.device_hash_reqs(wl.rows, dev)
+    out = torch.zeros(wl.out_len, dtype=torch.int64, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def go():
+        kvx.kvx_page_hashes(pay, wl.rec_bytes, wl.T, reqs, out, err)
+
+    for _ in range(args.warmup):
+        go()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        go()
+        e1.record(stream)
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    if int(err.item()):
+        log(f"device error bits {int(err.item())}")
+        return 1
+    nbytes = wl.payload_bytes()
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    kern_ms = sum(a.elapsed_time(b) for a, b in ev) / len(ev)
+    achieved = nbytes / (kern_ms / 1e3) / 1e9
+    cpu = None
+    if args.cpu_layers > 0:
+        from oracle import kvx_oracle
+        want = np.zeros(wl.out_len, np.uint64)
+        t2 = time.perf_counter()
+        e = kvx_oracle.default().page_hashes(pay_np, wl.rec_bytes, wl.T, wl.rows, want)
+        secs = time.perf_counter() - t2
+        exact = e == 0 and np.array_equal(out.cpu().numpy().view(np.uint64), want)
+        log(f"cpu oracle: {secs:.2f} s, bit-exact={exact}")
+        if not exact:
+            return 1
+        cpu = {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+               "sample": f"the whole workload ({nbytes / 1e6:.1f} MB of token ids), single-threaded",
+               "sample_bit_exact": exact, "cpu_model": _cpu_model(), "host_cpu_count": os.cpu_count()}
+    out_line = {
+        "metric": "chained page hash GB/s of payload, 1 MI355X", "value": round(nbytes / (ms_per_step / 1e3) / 1e9, 2),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u64", "data": "synthetic (seeded int32 token ids)",
+        "config": {"workload": wl.title, "name": wl.name, "requests": len(wl.rows),
+                   "positions": wl.positions, "pages": wl.out_len, "payload_bytes": nbytes},
+        "roofline": {"bound": "alu", "achieved": round(achieved, 2), "peak": round(HASH_PEAK_GBPS, 1),
+                     "unit": "GB/s", "frac": round(achieved / HASH_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "kvx page hashes", "bytes_per_launch": nbytes,
+                     "kernel_ms": round(kern_ms, 4)},
+        "cpu_baseline": cpu,
+        "context": {"kernel_sha": kernel_sha()},
+    }
+    print(json.dumps(out_line), flush=True)
     return 0
 
 

@@ -216,6 +216,35 @@ int kvx_scatter(const kvx_buf *src, const kvx_pool *dst,
                 const kvx_req *reqs, int32_t n_reqs,
                 uint32_t *dev_err, void *stream);
 
+/* One chained-hash request (32 bytes). */
+typedef struct kvx_hash_req {
+    int64_t payload_off;  /* first position of the request in the payload */
+    int64_t out_off;      /* index in `out` of the hash of the request's page 0 */
+    uint64_t seed;        /* chain state before page 0: 0 for a new chain, or the
+                             hash of the last full page of the prefix it extends */
+    int32_t n_positions;  /* positions of the request; 0 hashes nothing */
+    int32_t reserved;     /* must be 0 */
+} kvx_hash_req;
+
+/* Chained page hashes (Sec. 5.1: each page's hash encodes its predecessor's,
+ * so hashes are equal only when the whole prefix matches page by page).
+ * The paper names no hash function.  The definition used, with fnv =
+ * FNV-1a 64 (offset basis 0xcbf29ce484222325, prime 0x100000001b3):
+ *   page j of request r = its positions [j*T, min((j+1)*T, n)) of records
+ *                         of rec_bytes bytes (token ids, modality digests);
+ *   c_j = fnv(bytes of page j)
+ *   h_j = fnv(le64(h_{j-1}) || le64(c_j)),   h_{-1} = seed
+ *   out[out_off + j] = h_j for j < ceil(n / T).
+ * payload: device memory (or mapped pinned host memory), 4-byte aligned,
+ * payload_positions records.  rec_bytes: a positive multiple of 4.
+ * page_tokens: 1 .. KVX_MAX_PAGE_TOKENS.  out: out_len uint64 words,
+ * 8-byte aligned; requests must not share output words.  A record whose
+ * positions or outputs fall outside the arrays, with n_positions < 0 or a
+ * nonzero reserved word, is skipped and raises KVX_DERR_BAD_REQ. */
+int kvx_page_hashes(const void *payload, int64_t payload_positions, int32_t rec_bytes,
+                    int32_t page_tokens, const kvx_hash_req *reqs, int32_t n_reqs,
+                    uint64_t *out, int64_t out_len, uint32_t *dev_err, void *stream);
+
 /* Bytes a pool described by *pool occupies (-1 if the descriptor is invalid). */
 int64_t kvx_pool_bytes(const kvx_pool *pool);
 

@@ -15,8 +15,10 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libkvx.so")
-SOURCES = [os.path.join(CSRC, "kvx_kernels.hip"), os.path.join(CSRC, "kvx_api.cpp")]
-HEADERS = [os.path.join(INCLUDE, "kvx.h"), os.path.join(CSRC, "kvx_internal.h")]
+SOURCES = [os.path.join(CSRC, "kvx_kernels.hip"), os.path.join(CSRC, "kvx_hash.hip"),
+           os.path.join(CSRC, "kvx_api.cpp")]
+HEADERS = [os.path.join(INCLUDE, "kvx.h"), os.path.join(CSRC, "kvx_internal.h"),
+           os.path.join(CSRC, "kvx_hash.h")]
 ARCH = "gfx950"
 
 

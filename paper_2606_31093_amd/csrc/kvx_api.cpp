@@ -10,6 +10,7 @@
 #include <string>
 
 #include "kvx.h"
+#include "kvx_hash.h"
 #include "kvx_internal.h"
 
 namespace {
@@ -422,6 +423,58 @@ int kvx_transfer_layered(const kvx_pool *src, const kvx_pool *dst, const kvx_sli
         return fail(KVX_ERR_RANGE, "layers_per_group must be >= 1 (got %d)", layers_per_group);
     return transfer_impl(src, dst, slice, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
                          dev_err, stream, layers_per_group, events, n_events);
+}
+
+int kvx_page_hashes(const void *payload, int64_t payload_positions, int32_t rec_bytes,
+                    int32_t page_tokens, const kvx_hash_req *reqs, int32_t n_reqs, uint64_t *out,
+                    int64_t out_len, uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    if (rec_bytes < 4 || rec_bytes % 4 != 0)
+        return fail(KVX_ERR_SHAPE, "rec_bytes must be a positive multiple of 4 (got %d)", rec_bytes);
+    if (page_tokens < 1 || page_tokens > KVX_MAX_PAGE_TOKENS)
+        return fail(KVX_ERR_SHAPE, "page_tokens %d outside [1, %d]", page_tokens, KVX_MAX_PAGE_TOKENS);
+    if (payload_positions < 0 || out_len < 0)
+        return fail(KVX_ERR_RANGE, "payload_positions and out_len must be >= 0");
+    if (mul_checked(payload_positions, rec_bytes) < 0)
+        return fail(KVX_ERR_RANGE, "payload size exceeds 2^63 bytes");
+    if (n_reqs < 0 || n_reqs > KVX_MAX_REQS)
+        return fail(KVX_ERR_RANGE, "n_reqs %d outside [0, %d]", n_reqs, KVX_MAX_REQS);
+    if (n_reqs > 0 && !reqs) return fail(KVX_ERR_NULL, "reqs is NULL");
+    if (payload_positions > 0 && !payload) return fail(KVX_ERR_NULL, "payload is NULL");
+    if (out_len > 0 && !out) return fail(KVX_ERR_NULL, "out is NULL");
+    if ((reinterpret_cast<uintptr_t>(payload) & 3u) != 0)
+        return fail(KVX_ERR_ALIGN, "payload is not 4-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(out) & 7u) != 0 || (reinterpret_cast<uintptr_t>(reqs) & 7u) != 0)
+        return fail(KVX_ERR_ALIGN, "out and reqs must be 8-byte aligned");
+    if ((reinterpret_cast<uintptr_t>(dev_err) & 3u) != 0)
+        return fail(KVX_ERR_ALIGN, "dev_err is not 4-byte aligned");
+    if (n_reqs == 0) return KVX_OK;
+    kvx::HashParams P{};
+    void *d = nullptr;
+    int st;
+    if (payload_positions > 0) {
+        if ((st = device_view(payload, "payload", &d))) return st;
+        P.payload = static_cast<const uint32_t *>(d);
+    }
+    if (out_len > 0) {
+        if ((st = device_view(out, "out", &d))) return st;
+        P.out = static_cast<uint64_t *>(d);
+    }
+    if ((st = device_view(reqs, "reqs", &d))) return st;
+    P.reqs = static_cast<const kvx_hash_req *>(d);
+    if (dev_err) {
+        if ((st = device_view(dev_err, "dev_err", &d))) return st;
+        P.err = static_cast<uint32_t *>(d);
+    }
+    P.payload_positions = payload_positions;
+    P.rec_bytes = rec_bytes;
+    P.T = page_tokens;
+    P.n_reqs = n_reqs;
+    P.out_len = out_len;
+    const int e = kvx::launch_hash(P, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess)
+        return fail(KVX_ERR_HIP, "hash kernel launch failed: %s", hipGetErrorString((hipError_t)e));
+    return KVX_OK;
 }
 
 int64_t kvx_pool_bytes(const kvx_pool *pool) {

@@ -4,7 +4,8 @@ Every step of the copy runs in the library's HIP kernels.  PyTorch supplies
 device memory and the stream: tensors are passed as raw pointers and the
 kernels run on ``torch.cuda.current_stream()`` unless a stream is given.
 The functions keep the C names: ``kvx_transfer``, ``kvx_transfer_slice``,
-``kvx_transfer_layered``, ``kvx_gather`` and ``kvx_scatter``.  A missing or unloadable library raises; there is no
+``kvx_transfer_layered``, ``kvx_gather``, ``kvx_scatter`` and
+``kvx_page_hashes``.  A missing or unloadable library raises; there is no
 fallback path.
 
 Pool and buffer shapes are duck-typed: a pool shape has integer attributes
@@ -34,6 +35,10 @@ STATUS = {0: "KVX_OK", -1: "KVX_ERR_NULL", -2: "KVX_ERR_SHAPE", -3: "KVX_ERR_ALI
 REQ_DTYPE = np.dtype([("src_pt_off", "<i8"), ("dst_pt_off", "<i8"), ("buf_off", "<i8"),
                       ("src_start", "<i4"), ("dst_start", "<i4"), ("n_tokens", "<i4"),
                       ("reserved", "<i4")])
+
+
+HASH_REQ_DTYPE = np.dtype([("payload_off", "<i8"), ("out_off", "<i8"), ("seed", "<u8"),
+                           ("n_positions", "<i4"), ("reserved", "<i4")])
 
 
 class Pool(ctypes.Structure):
@@ -103,6 +108,8 @@ def lib() -> ctypes.CDLL:
         for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_transfer_layered, L.kvx_gather,
                   L.kvx_scatter):
             f.restype = ctypes.c_int
+        L.kvx_page_hashes.argtypes = [vp, i64, i32, i32, vp, i32, vp, i64, vp, vp]
+        L.kvx_page_hashes.restype = ctypes.c_int
         L.kvx_pool_bytes.argtypes = [pp]
         L.kvx_pool_bytes.restype = ctypes.c_int64
         L.kvx_strerror.argtypes = [ctypes.c_int]
@@ -282,6 +289,38 @@ def kvx_scatter(src, buf_spec, dst, dst_spec, dst_pt, reqs, dev_err=None, stream
     B, D = buf_desc(buf_spec, src), pool_desc(dst_spec, dst)
     _check(lib().kvx_scatter(ctypes.byref(B), ctypes.byref(D), _ptr(dst_pt), _len(dst_pt),
                              _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
+
+
+def pack_hash_reqs(rows) -> np.ndarray:
+    """(payload_off, out_off, seed, n_positions) rows -> kvx_hash_req records."""
+    rows = list(rows)
+    out = np.zeros(len(rows), dtype=HASH_REQ_DTYPE)
+    for i, (po, oo, seed, n) in enumerate(rows):
+        out[i] = (int(po), int(oo), int(seed) & 0xFFFFFFFFFFFFFFFF, int(n), 0)
+    return out
+
+
+def device_hash_reqs(rows, device="cuda"):
+    import torch
+    return torch.from_numpy(pack_hash_reqs(rows).view(np.uint8).copy()).to(device)
+
+
+def kvx_page_hashes(payload, rec_bytes, page_tokens, reqs, out, dev_err=None, stream=None) -> None:
+    """Chained page hashes (see kvx_page_hashes in include/kvx.h).  ``payload``
+    is a device tensor of records of ``rec_bytes`` bytes, ``reqs`` a device
+    tensor from ``device_hash_reqs``, ``out`` a 64-bit device tensor (one
+    word per page)."""
+    nbytes = payload.numel() * payload.element_size()
+    if nbytes % rec_bytes:
+        raise ValueError("payload is not a whole number of records")
+    if out.element_size() != 8 or not out.is_contiguous() or not payload.is_contiguous():
+        raise ValueError("out must be a contiguous 64-bit tensor; payload contiguous")
+    rb = reqs.numel() * reqs.element_size()
+    if rb % HASH_REQ_DTYPE.itemsize:
+        raise ValueError("reqs must hold whole 32-byte kvx_hash_req records")
+    _check(lib().kvx_page_hashes(_ptr(payload), nbytes // rec_bytes, int(rec_bytes),
+                                 int(page_tokens), _ptr(reqs), rb // HASH_REQ_DTYPE.itemsize,
+                                 _ptr(out), out.numel(), _ptr(dev_err), _stream(stream)))
 
 
 def kvx_strerror(status: int) -> str:

@@ -435,3 +435,49 @@ def init_sides_(wl: Workload, tensors: dict) -> None:
                 fill_random_bytes_(t, wl.value_seed)
         else:
             fill_prefill_(t, wl.prefill_tag)
+
+
+# --------------------------------------------------------------------------
+# chained page hashes (prefix matching, Sec. 5.1)
+# --------------------------------------------------------------------------
+
+@dataclass
+class HashWorkload:
+    name: str
+    title: str
+    rec_bytes: int               # bytes per position record (4: an int32 token id)
+    T: int                       # positions per page
+    positions: int               # records in the payload
+    rows: list                   # (payload_off, out_off, seed, n_positions)
+    out_len: int                 # hashes produced
+    payload_seed: int
+
+    def payload_bytes(self) -> int:
+        return self.positions * self.rec_bytes
+
+
+def page_hash(small: bool = False) -> HashWorkload:
+    """Prefix-matching hashes over token ids: 4096 requests with lengths
+    uniform in [1024, 8192] (64 in [1, 700] when small), 64-token pages,
+    int32 token ids; every eighth request continues the chain of the one
+    before it (seeded with a nonzero chain state), the rest start fresh."""
+    rng = np.random.default_rng(1108 if small else 1008)
+    nreq, lo, hi = (64, 1, 700) if small else (4096, 1024, 8192)
+    T = 64
+    lengths = rng.integers(lo, hi + 1, size=nreq)
+    seeds = rng.integers(1, 2**63, size=nreq)
+    rows, pos, out = [], 0, 0
+    for r, n in enumerate(lengths):
+        n = int(n)
+        seed = int(seeds[r]) if r % 8 == 7 else 0
+        rows.append((pos, out, seed, n))
+        pos += n
+        out += -(-n // T)
+    return HashWorkload("page_hash", f"chained page hashes, {nreq} requests of int32 token ids, "
+                        f"{T}-token pages", 4, T, pos, rows, out, payload_seed=2008)
+
+
+def hash_payload(wl: HashWorkload) -> np.ndarray:
+    """Token ids (uniform in [0, 2^17)) as int32 records."""
+    return np.random.default_rng(wl.payload_seed).integers(
+        0, 1 << 17, size=wl.positions * (wl.rec_bytes // 4), dtype=np.int32)

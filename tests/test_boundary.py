@@ -73,6 +73,9 @@ int main(void) {
   F(kvx_slice, src_kv0); F(kvx_slice, dst_kv0); F(kvx_slice, num_kv);
   F(kvx_slice, src_head0); F(kvx_slice, dst_head0); F(kvx_slice, num_heads);
   F(kvx_slice, reserved);
+  printf("kvx_hash_req %zu\n", sizeof(kvx_hash_req));
+  F(kvx_hash_req, payload_off); F(kvx_hash_req, out_off); F(kvx_hash_req, seed);
+  F(kvx_hash_req, n_positions); F(kvx_hash_req, reserved);
   return 0;
 }''')
     exe = tmp_path / "layout"
@@ -91,6 +94,9 @@ int main(void) {
         assert got[f"kvx_buf.{name}"] == getattr(kvx.Buf, name).offset
     for name in kvx.REQ_DTYPE.names:
         assert got[f"kvx_req.{name}"] == kvx.REQ_DTYPE.fields[name][1]
+    assert got["kvx_hash_req"] == kvx.HASH_REQ_DTYPE.itemsize
+    for name in kvx.HASH_REQ_DTYPE.names:
+        assert got[f"kvx_hash_req.{name}"] == kvx.HASH_REQ_DTYPE.fields[name][1]
     assert got["kvx_slice"] == ctypes.sizeof(kvx.Slice)
     for name, _ in kvx.Slice._fields_:
         assert got[f"kvx_slice.{name}"] == getattr(kvx.Slice, name).offset
@@ -218,6 +224,23 @@ def test_layered_host_validation(lib):
     assert call(2, None, 2) == -1               # no event array
     assert call(1, ev, 4) == -1                 # events[3] is NULL
     assert "events[3]" in kvx.kvx_last_error()
+
+
+@pytest.mark.parametrize("args,status", [
+    ((FAKE, 100, 4, 64, FAKE, 0, FAKE, 10), 0),            # nothing to hash
+    ((FAKE, 100, 6, 64, FAKE, 1, FAKE, 10), -2),           # records not whole words
+    ((FAKE, 100, 0, 64, FAKE, 1, FAKE, 10), -2),
+    ((FAKE, 100, 4, 0, FAKE, 1, FAKE, 10), -2),            # no page size
+    ((FAKE, -1, 4, 64, FAKE, 1, FAKE, 10), -5),
+    ((FAKE, 100, 4, 64, FAKE, -1, FAKE, 10), -5),
+    ((FAKE, 100, 4, 64, None, 1, FAKE, 10), -1),           # no records
+    ((None, 100, 4, 64, FAKE, 1, FAKE, 10), -1),           # no payload
+    ((FAKE, 100, 4, 64, FAKE, 1, None, 10), -1),           # no output
+    ((FAKE + 2, 100, 4, 64, FAKE, 1, FAKE, 10), -3),       # misaligned payload
+    ((FAKE, 100, 4, 64, FAKE, 1, FAKE + 4, 10), -3),       # misaligned output
+])
+def test_page_hash_host_validation(lib, args, status):
+    assert kvx.lib().kvx_page_hashes(*args, None, None) == status
 
 
 def test_slice_reserved_must_be_zero(lib):

@@ -1,0 +1,79 @@
+"""Chained page hashes on the GPU against the CPU oracle, word for word."""
+import numpy as np
+import pytest
+
+from paper_2606_31093_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    torch = pytest.importorskip("torch")
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_31093_amd import kvx
+    kvx.lib()
+    return torch
+
+
+def _both(torch, payload, rec_bytes, T, rows, out_len, raw=None):
+    from oracle import kvx_oracle
+    from paper_2606_31093_amd import kvx
+    want = np.full(out_len, 0x5A5A, np.uint64)
+    werr = kvx_oracle.default().page_hashes(payload, rec_bytes, T, rows, want)
+    p = torch.from_numpy(np.ascontiguousarray(payload).view(np.uint8).reshape(-1).copy()).cuda()
+    out = torch.full((out_len,), 0x5A5A, dtype=torch.int64, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    recs = raw if raw is not None else kvx.pack_hash_reqs(rows)
+    reqs = torch.from_numpy(recs.view(np.uint8).copy()).cuda()
+    kvx.kvx_page_hashes(p, rec_bytes, T, reqs, out, err)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy().view(np.uint64)
+    return got, int(err.item()), want, werr
+
+
+def test_small_workload(torch):
+    wl = W.page_hash(small=True)
+    pay = W.hash_payload(wl)
+    got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("rec_bytes", [4, 8, 12, 64])
+@pytest.mark.parametrize("T", [1, 3, 16, 64, 1000])
+def test_shapes(torch, rec_bytes, T):
+    rng = np.random.default_rng(rec_bytes * 1000 + T)
+    lengths = [0, 1, T - 1 if T > 1 else 2, T, T + 1, 5 * T + 3, 777]
+    rows, pos, out = [], 0, 0
+    for i, n in enumerate(lengths):
+        rows.append((pos, out, int(rng.integers(0, 2**63)) if i % 2 else 0, n))
+        pos += n
+        out += -(-n // T)
+    pay = rng.integers(0, 2**31, size=pos * rec_bytes // 4, dtype=np.int32)
+    got, gerr, want, werr = _both(torch, pay, rec_bytes, T, rows, out + 3)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
+
+
+def test_record_errors(torch):
+    pay = np.arange(40, dtype=np.int32)
+    rows = [(0, 0, 0, 40), (0, 4, 0, 41), (-1, 10, 0, 4), (0, 12, 0, -1), (30, 20, 0, 10)]
+    got, gerr, want, werr = _both(torch, pay, 4, 10, rows, 22)
+    assert gerr == werr == 8
+    assert np.array_equal(got, want)
+    from paper_2606_31093_amd import kvx
+    recs = kvx.pack_hash_reqs([(0, 0, 0, 40)])
+    recs["reserved"][0] = 1
+    got, gerr, _, _ = _both(torch, pay, 4, 10, [], 4, raw=recs)
+    assert gerr == 8 and (got == 0x5A5A).all()
+
+
+def test_full_workload(torch):
+    wl = W.page_hash()
+    pay = W.hash_payload(wl)
+    print(f"{wl.title}: {wl.positions} positions, {wl.out_len} pages", flush=True)
+    got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
