@@ -38,25 +38,27 @@ if ROOT not in sys.path:
 METRIC = "KV transfer GB/s (read+write) and % of HBM/host-link peak, 1 MI355X"
 HBM_PEAK_GBPS = 8000.0        # MI355X HBM3E, published
 PCIE_PEAK_GBPS = 63.0         # PCIe 5.0 x16 per direction: 32 GT/s x 16 x 128/130 / 8
-# The copy kernel and its launch shape; a change here invalidates the
-# committed HBM counter records.
-KERNEL_SOURCES = ["paper_2606_31093_amd/csrc/kvx_kernels.hip",
-                  "paper_2606_31093_amd/csrc/kvx_internal.h"]
+# Sources of each kernel and its launch shape; a change here invalidates the
+# committed HBM counter records of the workloads that run it.
+COPY_SOURCES = ["paper_2606_31093_amd/csrc/kvx_kernels.hip",
+                "paper_2606_31093_amd/csrc/kvx_internal.h"]
+HASH_SOURCES = ["paper_2606_31093_amd/csrc/kvx_hash.hip",
+                "paper_2606_31093_amd/csrc/kvx_hash.h"]
 
 
 def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def kernel_sha() -> str:
+def kernel_sha(workload: str = "handoff") -> str:
     h = hashlib.sha256()
-    for p in KERNEL_SOURCES:
+    for p in HASH_SOURCES if workload == "page_hash" else COPY_SOURCES:
         with open(os.path.join(ROOT, p), "rb") as f:
             h.update(f.read())
     return h.hexdigest()[:16]
 
 
-def traffic_record(key: int):
+def traffic_record(key: str):
     """HBM bytes per launch from the committed rocprofv3 counter summary,
     if it was taken on the current kernel sources."""
     path = os.path.join(ROOT, "profiles", f"traffic_{key}.json")
@@ -64,7 +66,7 @@ def traffic_record(key: int):
         return None
     with open(path) as f:
         rec = json.load(f)
-    if rec.get("kernel_sha") != kernel_sha():
+    if rec.get("kernel_sha") != kernel_sha(key):
         return None
     return rec
 
@@ -227,7 +229,8 @@ def main() -> int:
                     "kernel": f"kvx {dom.op}", "bytes_per_launch": int(dom_bytes),
                     "kernel_ms": round(kern_ms[i_dom], 4)}
 
-    context = {"kernel_sha": kernel_sha(), "per_step_kernel_ms": [round(x, 4) for x in kern_ms]}
+    context = {"kernel_sha": kernel_sha(args.workload),
+               "per_step_kernel_ms": [round(x, 4) for x in kern_ms]}
     for i, d in enumerate(dsteps):
         if d["events"]:
             # completion time of each layer group, from the start of the last timed step
@@ -385,6 +388,7 @@ def hash_bench(args) -> int:
         cpu = {"value": round(nbytes / secs / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
                "sample": f"the whole workload ({nbytes / 1e6:.1f} MB of token ids), single-threaded",
                "sample_bit_exact": exact, "cpu_model": _cpu_model(), "host_cpu_count": os.cpu_count()}
+    tr = traffic_record("page_hash")
     out_line = {
         "metric": "chained page hash GB/s of payload, 1 MI355X", "value": round(nbytes / (ms_per_step / 1e3) / 1e9, 2),
         "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -393,11 +397,12 @@ def hash_bench(args) -> int:
         "config": {"workload": wl.title, "name": wl.name, "requests": len(wl.rows),
                    "positions": wl.positions, "pages": wl.out_len, "payload_bytes": nbytes},
         "roofline": {"bound": "alu", "achieved": round(achieved, 2), "peak": round(HASH_PEAK_GBPS, 1),
-                     "unit": "GB/s", "frac": round(achieved / HASH_PEAK_GBPS, 4), "traffic": None,
+                     "unit": "GB/s", "frac": round(achieved / HASH_PEAK_GBPS, 4),
+                     "traffic": tr["traffic_bytes_per_launch"] if tr else None,
                      "kernel": "kvx page hashes", "bytes_per_launch": nbytes,
                      "kernel_ms": round(kern_ms, 4)},
         "cpu_baseline": cpu,
-        "context": {"kernel_sha": kernel_sha()},
+        "context": {"kernel_sha": kernel_sha("page_hash")},
     }
     print(json.dumps(out_line), flush=True)
     return 0
