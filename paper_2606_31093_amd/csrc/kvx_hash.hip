@@ -4,11 +4,13 @@
 //   c_j = fnv(records of page j),   h_j = fnv(le64(h_{j-1}) || le64(c_j)).
 //
 // One wavefront per request (a grid-stride loop over requests).  Pages are
-// taken 64 at a time: lane j computes the digest of page j of the chunk
-// (independent work, 16 word loads in flight per lane); then the chain runs
-// through the chunk's digests in page order, each broadcast from its lane,
-// and lane j keeps h_j, so the chunk's hashes leave in one coalesced store.
-// Nothing is allocated.
+// taken 64 at a time: lane j computes the digest of page j of the chunk,
+// issuing the loads of 64 words (a whole 256-byte page of token ids) before
+// hashing them, so the cache lines a page shares with its neighbours are
+// fetched while they are all in flight rather than once per batch.  The
+// chain then runs through the chunk's digests in page order, each broadcast
+// from its lane, and lane j keeps h_j, so the chunk's hashes leave in one
+// coalesced store.  Nothing is allocated.
 
 #include "kvx_hash.h"
 
@@ -16,6 +18,9 @@ namespace kvx {
 namespace {
 
 constexpr int kWave = 64;
+#ifndef KVX_HASH_BATCH
+#define KVX_HASH_BATCH 64   // words in flight per lane (measured: 16, 32, 64)
+#endif
 constexpr uint64_t kBasis = 0xcbf29ce484222325ull;
 constexpr uint64_t kPrime = 0x100000001b3ull;
 
@@ -33,16 +38,17 @@ __device__ __forceinline__ uint64_t fnv_u64(uint64_t h, uint64_t v) {
     return fnv_word(h, (uint32_t)(v >> 32));
 }
 
-// FNV-1a of nw 32-bit words, 16 loads in flight.
+// FNV-1a of nw 32-bit words, KVX_HASH_BATCH loads in flight.
 __device__ __forceinline__ uint64_t digest(const uint32_t *w, int64_t nw) {
+    constexpr int B = KVX_HASH_BATCH;
     uint64_t c = kBasis;
     int64_t i = 0;
-    for (; i + 16 <= nw; i += 16) {
-        uint32_t v[16];
+    for (; i + B <= nw; i += B) {
+        uint32_t v[B];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) v[u] = w[i + u];
+        for (int u = 0; u < B; ++u) v[u] = w[i + u];
 #pragma unroll
-        for (int u = 0; u < 16; ++u) c = fnv_word(c, v[u]);
+        for (int u = 0; u < B; ++u) c = fnv_word(c, v[u]);
     }
     for (; i < nw; ++i) c = fnv_word(c, w[i]);
     return c;
@@ -56,6 +62,7 @@ __device__ __forceinline__ uint64_t lane_u64(uint64_t v, int lane) {
 
 __global__ void __launch_bounds__(kWave) kvx_page_hash_kernel(HashParams p) {
     const int lane = threadIdx.x;
+    const int64_t wpr = p.rec_bytes / 4;
     for (int32_t r = blockIdx.x; r < p.n_reqs; r += gridDim.x) {
         const kvx_hash_req &q = p.reqs[r];
         const int64_t off = q.payload_off, out_off = q.out_off;
@@ -67,23 +74,22 @@ __global__ void __launch_bounds__(kWave) kvx_page_hash_kernel(HashParams p) {
             if (lane == 0 && p.err) atomicOr(p.err, KVX_DERR_BAD_REQ);
             continue;                       // uniform across the wavefront
         }
-        const int64_t wpr = p.rec_bytes / 4;
         uint64_t h = q.seed;                // uniform chain state
         for (int64_t j0 = 0; j0 < pages; j0 += kWave) {
+            const int in_chunk = pages - j0 < kWave ? (int)(pages - j0) : kWave;
             const int64_t j = j0 + lane;
             uint64_t c = 0;
-            if (j < pages) {
+            if (lane < in_chunk) {
                 const int64_t first = j * p.T;
                 const int64_t count = n - first < p.T ? n - first : p.T;
                 c = digest(p.payload + (off + first) * wpr, count * wpr);
             }
-            const int in_chunk = pages - j0 < kWave ? (int)(pages - j0) : kWave;
             uint64_t mine = 0;
             for (int k = 0; k < in_chunk; ++k) {
                 h = fnv_u64(fnv_u64(kBasis, h), lane_u64(c, k));
                 if (lane == k) mine = h;
             }
-            if (j < pages) p.out[out_off + j] = mine;
+            if (lane < in_chunk) p.out[out_off + j] = mine;
         }
     }
 }
