@@ -310,3 +310,13 @@ int main() {
     subprocess.run(cmd, check=True, capture_output=True)
     r = subprocess.run([str(exe)], capture_output=True, text=True)
     assert r.returncode == 0, r.stdout
+
+
+def test_missing_library_raises(monkeypatch, tmp_path):
+    """No fallback: a missing libkvx.so is an error, not a silent CPU path."""
+    monkeypatch.setattr(kvx, "_LIB", None)
+    monkeypatch.setenv("KVX_LIBRARY", str(tmp_path / "absent.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        kvx.lib()
+    with pytest.raises(RuntimeError):
+        kvx.kvx_abi_version()

@@ -210,6 +210,59 @@ def test_layered_records_events_when_empty():
 
 
 # ---------------------------------------------------------------------------
+# sizes at the edges
+# ---------------------------------------------------------------------------
+
+def test_huge_pages():
+    """Pages of 65536 tokens on both sides (tiles of 65536 rows), one page of
+    2^20 tokens read into smaller pages, and a head-major destination whose
+    rows are masked per page."""
+    check(cases.transfer_case("LPCTHD", "LPCTHD", 1 << 16, 1 << 16, seed=12, L=1, C=1, H=1, D=8,
+                              spec=[(5, 70000, 60000, None), (0, 0, 3, None)]))
+    check(cases.transfer_case("LPCTHD", "PLCHTD", 1 << 20, 4096, seed=13, L=1, C=1, H=2, D=8,
+                              spec=[(1000, 17, 9000, None)], extra_pages=1))
+
+
+def test_thousands_of_requests():
+    """4096 records, most of them tiny, some empty: every workgroup walks all
+    of them."""
+    rng = np.random.default_rng(21)
+    spec = [(int(rng.integers(0, 16)), int(rng.integers(0, 8)), int(rng.integers(0, 5)), None)
+            for _ in range(4096)]
+    check(cases.transfer_case("LPCTHD", "LPCTHD", 16, 8, seed=21, L=2, C=2, H=1, D=8, spec=spec,
+                              extra_pages=0))
+
+
+def test_graph_replays_match_eager():
+    """The transfer captured in a HIP graph and replayed several times, with
+    eager work in between, gives the eager result every time."""
+    import torch
+    from paper_2606_31093_amd import kvx
+    wl = get("handoff", small=True)
+    st = wl.steps[0]
+    init = initial_bytes(wl)
+    want, _ = run_oracle(wl, init)
+    a = torch.from_numpy(init["A"]).cuda()
+    b = torch.from_numpy(init["B"]).cuda()
+    spt, dpt, reqs = kvx.device_table(st.src_pt), kvx.device_table(st.dst_pt), kvx.device_reqs(st.reqs)
+    b0 = b.clone()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        kvx.kvx_transfer(a, wl.sides["A"], b, wl.sides["B"], spt, dpt, reqs, stream=s)   # warm up
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        kvx.kvx_transfer(a, wl.sides["A"], b, wl.sides["B"], spt, dpt, reqs)
+    for _ in range(3):
+        b.copy_(b0)                    # eager work between replays
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(b.cpu().numpy(), want["B"])
+
+
+# ---------------------------------------------------------------------------
 # error behaviour
 # ---------------------------------------------------------------------------
 
