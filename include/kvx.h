@@ -238,9 +238,13 @@ typedef struct kvx_hash_req {
  * payload: device memory (or mapped pinned host memory), 4-byte aligned,
  * payload_positions records.  rec_bytes: a positive multiple of 4.
  * page_tokens: 1 .. KVX_MAX_PAGE_TOKENS.  out: out_len uint64 words,
- * 8-byte aligned; requests must not share output words.  A record whose
- * positions or outputs fall outside the arrays, with n_positions < 0 or a
- * nonzero reserved word, is skipped and raises KVX_DERR_BAD_REQ. */
+ * 8-byte aligned; requests must not share output words, and out must not
+ * overlap the payload.  The call enqueues two kernels: the first writes the
+ * page digests c_j into out, the second replaces them with the chained
+ * hashes, so out holds final values only once the stream has passed both.
+ * A record whose positions or outputs fall outside the arrays, with
+ * n_positions < 0 or a nonzero reserved word, is skipped (its outputs are
+ * not written) and raises KVX_DERR_BAD_REQ. */
 int kvx_page_hashes(const void *payload, int64_t payload_positions, int32_t rec_bytes,
                     int32_t page_tokens, const kvx_hash_req *reqs, int32_t n_reqs,
                     uint64_t *out, int64_t out_len, uint32_t *dev_err, void *stream);

@@ -71,6 +71,9 @@ class LayerResult:
     equal: bool
     oracle_seconds: float
     moved_bytes: int      # algorithmic bytes (read + write) of this layer
+    # runs the same oracle call again on the same host arrays (the copy is
+    # idempotent), for timing several layers at once on several threads
+    rerun: object = dataclasses.field(default=None, repr=False)
 
 
 def check_transfer_layer(src_t, S, dst_t, D, step, l: int, tag: int,
@@ -87,11 +90,15 @@ def check_transfer_layer(src_t, S, dst_t, D, step, l: int, tag: int,
     else:
         want = pool_layer_prefill(D, l, tag)
         src = pool_layer(src_t, S, l)
+
+    def run() -> int:
+        return kvx_oracle.default().transfer(src, s1, want, d1, step.src_pt, step.dst_pt, step.reqs)
+
     t0 = time.perf_counter()
-    err = kvx_oracle.default().transfer(src, s1, want, d1, step.src_pt, step.dst_pt, step.reqs)
+    err = run()
     dt = time.perf_counter() - t0
     moved = 2 * int(step.reqs[:, 5].sum()) * S.C * S.H * S.D * S.e
-    return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved)
+    return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved, run)
 
 
 def check_transfer_slice_layer(src_t, S, dst_t, D, step, l: int, tag: int) -> LayerResult:
@@ -104,12 +111,16 @@ def check_transfer_slice_layer(src_t, S, dst_t, D, step, l: int, tag: int) -> La
     got = pool_layer(dst_t, D, ld)
     want = pool_layer_prefill(D, ld, tag)
     one = [0, 0, 1] + sl[3:]
+
+    def run() -> int:
+        return kvx_oracle.default().transfer_slice(src, s1, want, d1, one, step.src_pt,
+                                                   step.dst_pt, step.reqs)
+
     t0 = time.perf_counter()
-    err = kvx_oracle.default().transfer_slice(src, s1, want, d1, one, step.src_pt, step.dst_pt,
-                                               step.reqs)
+    err = run()
     dt = time.perf_counter() - t0
     moved = 2 * int(step.reqs[:, 5].sum()) * sl[5] * sl[8] * S.D * S.e
-    return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved)
+    return LayerResult(l, err == 0 and np.array_equal(got, want), dt, moved, run)
 
 
 def gather_scatter_layer(pool_before: np.ndarray, S, buf_t, B, pool_after: np.ndarray,

@@ -3,14 +3,25 @@
 // prefix page by page).  Definition, with fnv = FNV-1a 64:
 //   c_j = fnv(records of page j),   h_j = fnv(le64(h_{j-1}) || le64(c_j)).
 //
-// One wavefront per request (a grid-stride loop over requests).  Pages are
-// taken 64 at a time: lane j computes the digest of page j of the chunk,
-// issuing the loads of 64 words (a whole 256-byte page of token ids) before
-// hashing them, so the cache lines a page shares with its neighbours are
-// fetched while they are all in flight rather than once per batch.  The
-// chain then runs through the chunk's digests in page order, each broadcast
-// from its lane, and lane j keeps h_j, so the chunk's hashes leave in one
-// coalesced store.  Nothing is allocated.
+// Two launches on the caller's stream, nothing allocated:
+//
+// 1. Digests.  One wavefront per request (a grid-stride loop over
+//    requests); pages are taken 64 at a time and lane j computes c_j,
+//    issuing the loads of 64 words (a whole 256-byte page of token ids)
+//    before hashing them, so the cache lines a page shares with its
+//    neighbours are fetched while they are all in flight.  c_j goes to
+//    out[out_off + j], 64 pages per coalesced store.  This is where the
+//    arithmetic is: 256 bytes hashed per page.
+//
+// 2. Chain.  One lane per request: the lane walks its request's digests in
+//    page order and overwrites each with h_j.  16 bytes hashed per page, but
+//    strictly in order.  With a lane per request the chain costs one vector
+//    instruction stream per 64 requests; run inside the digest wavefronts it
+//    would be one scalar instruction stream per request, and the scalar unit
+//    a compute unit's wavefronts share becomes the bottleneck.
+//
+// Between the two launches out[] holds the digests: callers see it only
+// after the stream has passed both.
 
 #include "kvx_hash.h"
 
@@ -19,7 +30,10 @@ namespace {
 
 constexpr int kWave = 64;
 #ifndef KVX_HASH_BATCH
-#define KVX_HASH_BATCH 64   // words in flight per lane (measured: 16, 32, 64)
+#define KVX_HASH_BATCH 32   // words in flight per lane in the digest
+#endif
+#ifndef KVX_CHAIN_BATCH
+#define KVX_CHAIN_BATCH 16  // digests in flight per lane in the chain
 #endif
 constexpr uint64_t kBasis = 0xcbf29ce484222325ull;
 constexpr uint64_t kPrime = 0x100000001b3ull;
@@ -38,6 +52,11 @@ __device__ __forceinline__ uint64_t fnv_u64(uint64_t h, uint64_t v) {
     return fnv_word(h, (uint32_t)(v >> 32));
 }
 
+// h_j from h_{j-1} and c_j.
+__device__ __forceinline__ uint64_t chain_step(uint64_t h, uint64_t c) {
+    return fnv_u64(fnv_u64(kBasis, h), c);
+}
+
 // FNV-1a of nw 32-bit words, KVX_HASH_BATCH loads in flight.
 __device__ __forceinline__ uint64_t digest(const uint32_t *w, int64_t nw) {
     constexpr int B = KVX_HASH_BATCH;
@@ -54,42 +73,62 @@ __device__ __forceinline__ uint64_t digest(const uint32_t *w, int64_t nw) {
     return c;
 }
 
-__device__ __forceinline__ uint64_t lane_u64(uint64_t v, int lane) {
-    const uint32_t lo = __builtin_amdgcn_readlane((int)(uint32_t)v, lane);
-    const uint32_t hi = __builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
-    return ((uint64_t)hi << 32) | lo;
+// A record is used only if its payload range and its out range lie inside
+// the caller's buffers; *pages receives its page count.
+__device__ __forceinline__ bool valid(const kvx_hash_req &q, const HashParams &p,
+                                      int64_t *pages) {
+    const int32_t n = q.n_positions;
+    *pages = n > 0 ? ((int64_t)n + p.T - 1) / p.T : 0;
+    return n >= 0 && q.reserved == 0 && q.payload_off >= 0 &&
+           q.payload_off <= p.payload_positions - n && q.out_off >= 0 &&
+           q.out_off <= p.out_len - *pages;
 }
 
-__global__ void __launch_bounds__(kWave) kvx_page_hash_kernel(HashParams p) {
+__global__ void __launch_bounds__(kWave) kvx_page_digest_kernel(HashParams p) {
     const int lane = threadIdx.x;
     const int64_t wpr = p.rec_bytes / 4;
     for (int32_t r = blockIdx.x; r < p.n_reqs; r += gridDim.x) {
         const kvx_hash_req &q = p.reqs[r];
-        const int64_t off = q.payload_off, out_off = q.out_off;
-        const int32_t n = q.n_positions;
-        const int64_t pages = n > 0 ? ((int64_t)n + p.T - 1) / p.T : 0;
-        const bool ok = n >= 0 && q.reserved == 0 && off >= 0 && off <= p.payload_positions - n &&
-                        out_off >= 0 && out_off <= p.out_len - pages;
-        if (!ok) {
+        int64_t pages;
+        if (!valid(q, p, &pages)) {
             if (lane == 0 && p.err) atomicOr(p.err, KVX_DERR_BAD_REQ);
             continue;                       // uniform across the wavefront
         }
-        uint64_t h = q.seed;                // uniform chain state
-        for (int64_t j0 = 0; j0 < pages; j0 += kWave) {
-            const int in_chunk = pages - j0 < kWave ? (int)(pages - j0) : kWave;
-            const int64_t j = j0 + lane;
-            uint64_t c = 0;
-            if (lane < in_chunk) {
-                const int64_t first = j * p.T;
-                const int64_t count = n - first < p.T ? n - first : p.T;
-                c = digest(p.payload + (off + first) * wpr, count * wpr);
+        const int32_t n = q.n_positions;
+        for (int64_t j = lane; j < pages; j += kWave) {
+            const int64_t first = j * p.T;
+            const int64_t count = n - first < p.T ? n - first : p.T;
+            p.out[q.out_off + j] = digest(p.payload + (q.payload_off + first) * wpr, count * wpr);
+        }
+    }
+}
+
+__global__ void __launch_bounds__(kWave) kvx_page_chain_kernel(HashParams p) {
+    constexpr int B = KVX_CHAIN_BATCH;
+    for (int64_t r = (int64_t)blockIdx.x * kWave + threadIdx.x; r < p.n_reqs;
+         r += (int64_t)gridDim.x * kWave) {
+        const kvx_hash_req &q = p.reqs[r];
+        int64_t pages;
+        if (!valid(q, p, &pages)) continue;     // flagged by the digest launch
+        uint64_t *o = p.out + q.out_off;
+        uint64_t h = q.seed;
+        uint64_t next[B];
+#pragma unroll
+        for (int u = 0; u < B; ++u) next[u] = u < pages ? o[u] : 0;
+        for (int64_t j = 0; j < pages; j += B) {
+            uint64_t c[B];
+#pragma unroll
+            for (int u = 0; u < B; ++u) c[u] = next[u];
+            // the following batch is in flight while this one is chained
+#pragma unroll
+            for (int u = 0; u < B; ++u) next[u] = j + B + u < pages ? o[j + B + u] : 0;
+#pragma unroll
+            for (int u = 0; u < B; ++u) {
+                if (j + u < pages) {
+                    h = chain_step(h, c[u]);
+                    o[j + u] = h;
+                }
             }
-            uint64_t mine = 0;
-            for (int k = 0; k < in_chunk; ++k) {
-                h = fnv_u64(fnv_u64(kBasis, h), lane_u64(c, k));
-                if (lane == k) mine = h;
-            }
-            if (lane < in_chunk) p.out[out_off + j] = mine;
         }
     }
 }
@@ -97,13 +136,19 @@ __global__ void __launch_bounds__(kWave) kvx_page_hash_kernel(HashParams p) {
 }  // namespace
 
 int launch_hash(const HashParams &p, hipStream_t stream) {
+    if (p.n_reqs == 0) return hipSuccess;
     int dev = 0, cus = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
-    const int grid = p.n_reqs < cus * 32 ? p.n_reqs : cus * 32;
-    hipLaunchKernelGGL(kvx_page_hash_kernel, dim3(grid), dim3(kWave), 0, stream, p);
+    const int digest_grid = p.n_reqs < cus * 32 ? p.n_reqs : cus * 32;
+    hipLaunchKernelGGL(kvx_page_digest_kernel, dim3(digest_grid), dim3(kWave), 0, stream, p);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const int chain_blocks = (p.n_reqs + kWave - 1) / kWave;
+    const int chain_grid = chain_blocks < cus * 8 ? chain_blocks : cus * 8;
+    hipLaunchKernelGGL(kvx_page_chain_kernel, dim3(chain_grid), dim3(kWave), 0, stream, p);
     return hipGetLastError();
 }
 
