@@ -12,9 +12,12 @@
 // layer l); the tiling side is the destination pool for transfer and
 // scatter (each tile then writes one destination page of one layer, and no
 // two tiles write the same bytes) and the source pool for gather.  A
-// persistent grid of workgroups strides over the flat tile index; each
-// workgroup walks the request records in order, keeping a running tile
-// count, so no tile table or scratch memory is needed.
+// persistent grid of workgroups strides over the flat tile index.  Each
+// workgroup reads the request records 256 at a time, one per thread, turns
+// their tile counts into tile ranges with a scan in LDS and finds the record
+// of each of its tiles by binary search, so no tile table or scratch memory
+// is needed and thousands of small requests cost a few parallel loads per
+// chunk rather than a chain of dependent ones.
 //
 // Inside a tile the tiling side's rows are a fixed page of one layer.  The
 // other side's rows come from one or more of its pages ("pieces"), whose ids
@@ -336,20 +339,59 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
     copy_rows<OP, TTHD, KVX_UNROLL_ROWS>(p, q, t);
 }
 
+// Inclusive sum of x over the workgroup's threads (x = 0 past the chunk).
+// Every thread of the workgroup must call it: it contains barriers.
+__device__ __forceinline__ int64_t block_scan(int64_t x, int64_t *s_wave) {
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+#pragma unroll
+    for (int d = 1; d < kWave; d <<= 1) {
+        const int64_t y = __shfl_up(x, d, kWave);
+        if (lane >= d) x += y;
+    }
+    if (lane == kWave - 1) s_wave[wid] = x;
+    __syncthreads();
+    for (int w = 0; w < wid; ++w) x += s_wave[w];
+    return x;
+}
+
 template <int OP, bool TTHD>
 __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
+    // Records are taken kBlock at a time: each thread reads one and counts
+    // its tiles, a workgroup scan turns the counts into tile ranges, and the
+    // workgroup's tiles inside the chunk find their record by binary search.
+    __shared__ int64_t s_end[kBlock];   // end (exclusive) of record i's tiles in the chunk
+    __shared__ int64_t s_wave[kBlock / kWave];
     Req q;
-    int32_t r = -1;
-    int64_t base = 0, cnt = 0;
-    for (int64_t tile = blockIdx.x;; tile += gridDim.x) {
-        while (tile >= base + cnt) {
-            base += cnt;
-            if (++r >= p.n_reqs) return;
-            if (!load_req<OP>(p, r, q) && blockIdx.x == 0 && threadIdx.x == 0)
+    int32_t cached = -1;
+    int64_t tile = blockIdx.x, chunk_base = 0;
+    for (int32_t r0 = 0; r0 < p.n_reqs; r0 += kBlock) {
+        const int32_t nr = p.n_reqs - r0 < kBlock ? p.n_reqs - r0 : kBlock;
+        int64_t cnt = 0;
+        if ((int32_t)threadIdx.x < nr) {
+            Req mine;
+            if (!load_req<OP>(p, r0 + threadIdx.x, mine) && blockIdx.x == 0)
                 report(p, KVX_DERR_BAD_REQ);
-            cnt = q.tiles;
+            cnt = mine.tiles;
         }
-        do_tile<OP, TTHD>(p, q, tile - base);
+        s_end[threadIdx.x] = block_scan(cnt, s_wave);
+        __syncthreads();
+        const int64_t chunk_tiles = s_end[kBlock - 1];
+        for (; tile < chunk_base + chunk_tiles; tile += gridDim.x) {
+            const int64_t local = tile - chunk_base;
+            int32_t lo = 0, hi = nr - 1;             // first record whose range ends past `local`
+            while (lo < hi) {
+                const int32_t mid = (lo + hi) >> 1;
+                if (s_end[mid] > local) hi = mid;
+                else lo = mid + 1;
+            }
+            if (r0 + lo != cached) {
+                load_req<OP>(p, r0 + lo, q);
+                cached = r0 + lo;
+            }
+            do_tile<OP, TTHD>(p, q, local - (lo ? s_end[lo - 1] : 0));
+        }
+        chunk_base += chunk_tiles;
+        __syncthreads();                             // s_end and s_wave are rewritten next chunk
     }
 }
 

@@ -77,3 +77,30 @@ def test_full_workload(torch):
     got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
     assert gerr == werr == 0
     assert np.array_equal(got, want)
+
+
+def test_chain_lengths_and_scattered_outputs(torch):
+    """Page counts around every multiple of the chain's and the digest's
+    batches (16 digests, 64 pages), 300 requests so that the chain spans
+    several wavefronts with lanes of very different lengths, outputs placed
+    in a shuffled order with gaps, and requests that reread the same
+    payload."""
+    rng = np.random.default_rng(77)
+    T = 4
+    pages = [1, 15, 16, 17, 31, 32, 33, 63, 64, 65, 127, 128, 129, 200]
+    pages = pages + [int(p) for p in rng.integers(0, 150, size=300 - len(pages))]
+    n = [max(0, p * T - int(rng.integers(0, T))) if p else 0 for p in pages]
+    slots = rng.permutation(len(n))
+    out_offs, cursor = [0] * len(n), 5
+    for i in slots:                      # outputs in a shuffled order, with gaps
+        out_offs[i] = cursor
+        cursor += -(-n[i] // T) + int(rng.integers(0, 3))
+    total = sum(n)
+    rows = []
+    for i, k in enumerate(n):
+        off = int(rng.integers(0, total - k + 1)) if i % 3 == 0 else sum(n[:i])
+        rows.append((off, out_offs[i], int(rng.integers(0, 2**63)) if i % 4 else 0, k))
+    pay = rng.integers(0, 2**31, size=total, dtype=np.int32)
+    got, gerr, want, werr = _both(torch, pay, 4, T, rows, cursor + 7)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
