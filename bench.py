@@ -78,7 +78,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="handoff",
                     choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
-                             "handoff_layered", "page_hash"])
+                             "handoff_layered", "small_requests", "page_hash"])
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="layers of the workload the CPU oracle runs (0: skip)")
     ap.add_argument("--cpu-threads", type=int, default=16,

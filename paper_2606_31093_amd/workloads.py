@@ -319,8 +319,36 @@ def handoff_layered(small: bool = False) -> Workload:
     return wl
 
 
+def small_requests(small: bool = False) -> Workload:
+    """Many tiny requests at once, as when the newest tokens of every running
+    sequence move after a decode step (Sec. 4.1.4: partial pages keep their
+    other slots).  16384 requests (256 when small), each moving 1 to 4 tokens
+    from a random slot range of a random source page into its own 4-slot
+    group of a destination page; 16 groups per 64-token page, so no two
+    requests write the same slot.  Pools as in the handoff."""
+    if small:
+        rng = np.random.default_rng(1112)
+        L, H, N, nreq = 3, 2, 64, 256
+    else:
+        rng = np.random.default_rng(1012)
+        L, H, N, nreq = 36, 8, 4096, 16384
+    T, group = 64, 4
+    pool = PoolSpec(L, 2, H, 128, T=T, N=N, e=2, layout="LPCTHD")
+    n = rng.integers(1, group + 1, size=nreq)
+    src_pt = rng.integers(0, N, size=nreq).astype(np.int32)
+    s0 = np.array([rng.integers(0, T - k + 1) for k in n])
+    slots = rng.permutation(N * (T // group))[:nreq]          # distinct (page, group) pairs
+    dst_pt = (slots // (T // group)).astype(np.int32)
+    d0 = (slots % (T // group)) * group
+    rows = [[r, r, 0, int(s0[r]), int(d0[r]), int(n[r])] for r in range(nreq)]
+    step = Step("transfer", "A", "B", src_pt, dst_pt, _reqs(rows))
+    return Workload("small_requests", f"{nreq} small requests (1-{group} tokens each), "
+                    f"{L}L x {H}H x 128, 64-token pages", {"A": pool, "B": pool}, [step],
+                    value_seed=2012, prefill_tag=12)
+
+
 NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
-         "handoff_layered")
+         "handoff_layered", "small_requests")
 
 
 def get(name: str, small: bool = False) -> Workload:
@@ -329,7 +357,8 @@ def get(name: str, small: bool = False) -> Workload:
         return tiny()
     return {"handoff": handoff, "relayout": relayout, "mla": mla,
             "host_tier": host_tier, "tp_reshard": tp_reshard,
-            "cow_fork": cow_fork, "handoff_layered": handoff_layered}[name](small=small)
+            "cow_fork": cow_fork, "handoff_layered": handoff_layered,
+            "small_requests": small_requests}[name](small=small)
 
 
 def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:

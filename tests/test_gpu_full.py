@@ -54,7 +54,8 @@ def _free(torch, *objs):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("k", ["handoff", "relayout", "mla", "tp_reshard", "cow_fork"])
+@pytest.mark.parametrize("k", ["handoff", "relayout", "mla", "tp_reshard", "cow_fork",
+                               "small_requests"])
 def test_full_transfer(torch, k):
     from oracle import layer_check
     wl, mem, dsteps = _setup(torch, k)

@@ -36,7 +36,7 @@ def test_tiny_workload():
 
 
 @pytest.mark.parametrize("name", ["handoff", "relayout", "mla", "host_tier", "tp_reshard",
-                                  "cow_fork", "handoff_layered"])
+                                  "cow_fork", "handoff_layered", "small_requests"])
 def test_small_workloads(name):
     check(get(name, small=True))
 

@@ -40,6 +40,24 @@ def test_tables_cover_and_destinations_are_disjoint(k, small):
         assert len(np.unique(st.dst_pt)) == len(st.dst_pt) if st.dst_pt is not None else True
 
 
+@pytest.mark.parametrize("small", [False, True])
+def test_small_requests_write_disjoint_slots(small):
+    """Requests share destination pages but never a destination slot, and
+    each request's tokens lie inside one page on both sides."""
+    wl = W.get("small_requests", small=small)
+    st = wl.steps[0]
+    P = wl.sides["A"]
+    cells = set()
+    for so, do, bo, s0, d0, n in st.reqs:
+        assert 1 <= n <= 4 and s0 + n <= P.T and d0 + n <= P.T
+        assert 0 <= st.src_pt[so] < P.N and 0 <= st.dst_pt[do] < P.N
+        for q in range(d0, d0 + n):
+            cell = (int(st.dst_pt[do]), int(q))
+            assert cell not in cells
+            cells.add(cell)
+    assert len(st.reqs) == (256 if small else 16384)
+
+
 def test_deterministic():
     for k in W.NAMES:
         a, b = W.get(k), W.get(k)
