@@ -17,7 +17,9 @@
 // their tile counts into tile ranges with a scan in LDS and finds the record
 // of each of its tiles by binary search, so no tile table or scratch memory
 // is needed and thousands of small requests cost a few parallel loads per
-// chunk rather than a chain of dependent ones.
+// chunk rather than a chain of dependent ones.  A tile is copied by one
+// worker: a wavefront when the launch copies contiguous runs (four small
+// tiles in flight per workgroup), the whole workgroup when it resolves rows.
 //
 // Inside a tile the tiling side's rows are a fixed page of one layer.  The
 // other side's rows come from one or more of its pages ("pieces"), whose ids
@@ -53,12 +55,22 @@
 #ifndef KVX_BLOCK
 #define KVX_BLOCK 256
 #endif
+#ifndef KVX_FLAT_WAVE_TILES
+#define KVX_FLAT_WAVE_TILES 1  // launches of contiguous runs: one tile per wavefront
+#endif
+#ifndef KVX_ROWS_WAVE_TILES
+#define KVX_ROWS_WAVE_TILES 0  // launches that resolve rows: one tile per workgroup
+#endif
 
 namespace kvx {
 namespace {
 
 constexpr int kBlock = KVX_BLOCK;
 constexpr int kWave = 64;
+// A worker copies one tile at a time: a wavefront or the whole workgroup,
+// NT threads (a template parameter below).
+template <int NT>
+__device__ __forceinline__ uint32_t worker_tid() { return threadIdx.x % NT; }
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
@@ -132,16 +144,16 @@ __device__ __forceinline__ bool load_req(const Params &p, int32_t r, Req &q) {
     return true;
 }
 
-// Plain vector stream over C runs of R vectors each.
-template <int U>
+// Plain vector stream over C runs of R vectors each, by a worker of NT threads.
+template <int NT, int U>
 __device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, int64_t s_sc,
                                           uint32_t R, int32_t C) {
     const uint32_t total = R * (uint32_t)C;
-    for (uint32_t k0 = threadIdx.x; k0 < total; k0 += kBlock * U) {
+    for (uint32_t k0 = worker_tid<NT>(); k0 < total; k0 += NT * U) {
         v4u v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const uint32_t k = k0 + u * kBlock;
+            const uint32_t k = k0 + u * NT;
             if (k < total) {
                 const uint32_t c = k >= R;
                 const uint32_t w = k - c * R;
@@ -150,7 +162,7 @@ __device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, 
         }
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const uint32_t k = k0 + u * kBlock;
+            const uint32_t k = k0 + u * NT;
             if (k < total) {
                 const uint32_t c = k >= R;
                 const uint32_t w = k - c * R;
@@ -178,7 +190,7 @@ struct Tile {
 // General row-resolving copy.  Vectors are enumerated in the tiling side's
 // memory order: (c, slot, h, v) when it is token-major, else (c, h, slot, v)
 // over whole pages with the slots outside [sa, sb) masked.
-template <int OP, bool TTHD, int U>
+template <int OP, bool TTHD, int NT, int U>
 __device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const Tile &t) {
     constexpr bool kTileSrc = OP == OP_GATHER;
     constexpr bool kOtherBuf = OP != OP_TRANSFER;
@@ -188,13 +200,15 @@ __device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const T
     const uint32_t rows_c = TTHD ? (uint32_t)t.ntok * H : H * (uint32_t)ts.T;
     const uint32_t total = rows_c * vpr * (uint32_t)p.C;
     const char *o_l = os.base + (int64_t)t.l * os.s_l;
-    for (uint32_t k0 = threadIdx.x; k0 < total; k0 += kBlock * U) {
+    // The trip count is the same for every lane: the page-id broadcast below
+    // reads other lanes, which must all still be active.
+    for (uint32_t kb = 0; kb < total; kb += NT * U) {
         const char *src[U];
         char *dst[U];
         bool ok[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
-            const uint32_t kk = k0 + u * kBlock;
+            const uint32_t kk = kb + worker_tid<NT>() + u * NT;
             const uint32_t k = kk < total ? kk : total - 1;
             bool valid = kk < total;
             const uint32_t rw = fd_div(p.fd_vpr, k);
@@ -253,7 +267,7 @@ __device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const T
     }
 }
 
-template <int OP, bool TTHD>
+template <int OP, bool TTHD, int NT>
 __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t local) {
     constexpr bool kTileSrc = OP == OP_GATHER;
     constexpr bool kOtherBuf = OP != OP_TRANSFER;
@@ -275,12 +289,12 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
     // Tiling-side page (one per tile; a uniform load).
     const int64_t tidx = q.t_pt_off + j;
     if (tidx < 0 || tidx >= ts.pt_len) {
-        if (threadIdx.x == 0) report(p, KVX_DERR_PT_RANGE);
+        if (worker_tid<NT>() == 0) report(p, KVX_DERR_PT_RANGE);
         return;
     }
     const int32_t tpage = ts.pt[tidx];
     if (tpage < 0 || tpage >= ts.N) {
-        if (threadIdx.x == 0) report(p, kTileSrc ? KVX_DERR_SRC_PAGE : KVX_DERR_DST_PAGE);
+        if (worker_tid<NT>() == 0) report(p, kTileSrc ? KVX_DERR_SRC_PAGE : KVX_DERR_DST_PAGE);
         return;
     }
     t.t_base = ts.base + (int64_t)t.l * ts.s_l + (int64_t)tpage * ts.s_p;
@@ -297,10 +311,10 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
         if (p.flat) {
             const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
             if (kTileSrc)
-                copy_runs<KVX_UNROLL_FLAT>(const_cast<char *>(t.o_row0), tb, t.o_sc, ts.s_c,
+                copy_runs<NT, KVX_UNROLL_FLAT>(const_cast<char *>(t.o_row0), tb, t.o_sc, ts.s_c,
                                            (uint32_t)run_t, p.C);
             else
-                copy_runs<KVX_UNROLL_FLAT>(const_cast<char *>(tb), t.o_row0, ts.s_c, t.o_sc,
+                copy_runs<NT, KVX_UNROLL_FLAT>(const_cast<char *>(tb), t.o_row0, ts.s_c, t.o_sc,
                                            (uint32_t)run_t, p.C);
             return;
         }
@@ -322,7 +336,7 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
                 if (id < 0 || id >= os.N) bad = KVX_DERR_SRC_PAGE;
                 else t.pid = id;
             }
-            if (bad && threadIdx.x < kWave) report(p, bad);
+            if (bad && worker_tid<NT>() < kWave) report(p, bad);   // the worker's first wavefront
         }
         if (p.flat && K == 1) {
             const int32_t pg = __builtin_amdgcn_readfirstlane(t.pid);
@@ -331,12 +345,12 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
             const char *ob = os.base + (int64_t)t.l * os.s_l + (int64_t)pg * os.s_p +
                              (int64_t)so0 * os.s_t;
             const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
-            copy_runs<KVX_UNROLL_FLAT>(const_cast<char *>(tb), ob, ts.s_c, os.s_c,
+            copy_runs<NT, KVX_UNROLL_FLAT>(const_cast<char *>(tb), ob, ts.s_c, os.s_c,
                                        (uint32_t)run_t, p.C);
             return;
         }
     }
-    copy_rows<OP, TTHD, KVX_UNROLL_ROWS>(p, q, t);
+    copy_rows<OP, TTHD, NT, KVX_UNROLL_ROWS>(p, q, t);
 }
 
 // Inclusive sum of x over the workgroup's threads (x = 0 past the chunk).
@@ -354,8 +368,9 @@ __device__ __forceinline__ int64_t block_scan(int64_t x, int64_t *s_wave) {
     return x;
 }
 
-template <int OP, bool TTHD>
+template <int OP, bool TTHD, int NT>
 __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
+    constexpr int kWorkers = kBlock / NT;
     // Records are taken kBlock at a time: each thread reads one and counts
     // its tiles, a workgroup scan turns the counts into tile ranges, and the
     // workgroup's tiles inside the chunk find their record by binary search.
@@ -363,7 +378,8 @@ __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
     __shared__ int64_t s_wave[kBlock / kWave];
     Req q;
     int32_t cached = -1;
-    int64_t tile = blockIdx.x, chunk_base = 0;
+    const int64_t stride = (int64_t)gridDim.x * kWorkers;
+    int64_t tile = (int64_t)blockIdx.x * kWorkers + threadIdx.x / NT, chunk_base = 0;
     for (int32_t r0 = 0; r0 < p.n_reqs; r0 += kBlock) {
         const int32_t nr = p.n_reqs - r0 < kBlock ? p.n_reqs - r0 : kBlock;
         int64_t cnt = 0;
@@ -376,7 +392,7 @@ __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
         s_end[threadIdx.x] = block_scan(cnt, s_wave);
         __syncthreads();
         const int64_t chunk_tiles = s_end[kBlock - 1];
-        for (; tile < chunk_base + chunk_tiles; tile += gridDim.x) {
+        for (; tile < chunk_base + chunk_tiles; tile += stride) {   // uniform per worker
             const int64_t local = tile - chunk_base;
             int32_t lo = 0, hi = nr - 1;             // first record whose range ends past `local`
             while (lo < hi) {
@@ -388,7 +404,7 @@ __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
                 load_req<OP>(p, r0 + lo, q);
                 cached = r0 + lo;
             }
-            do_tile<OP, TTHD>(p, q, local - (lo ? s_end[lo - 1] : 0));
+            do_tile<OP, TTHD, NT>(p, q, local - (lo ? s_end[lo - 1] : 0));
         }
         chunk_base += chunk_tiles;
         __syncthreads();                             // s_end and s_wave are rewritten next chunk
@@ -397,14 +413,21 @@ __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
 
 typedef void (*KernelFn)(Params);
 
-KernelFn pick(int op, bool tthd) {
+constexpr int kFlatNT = KVX_FLAT_WAVE_TILES ? kWave : kBlock;
+constexpr int kRowsNT = KVX_ROWS_WAVE_TILES ? kWave : kBlock;
+
+template <int OP>
+KernelFn pick_op(bool tthd, bool flat) {
+    if (flat)
+        return tthd ? kvx_copy_kernel<OP, true, kFlatNT> : kvx_copy_kernel<OP, false, kFlatNT>;
+    return tthd ? kvx_copy_kernel<OP, true, kRowsNT> : kvx_copy_kernel<OP, false, kRowsNT>;
+}
+
+KernelFn pick(int op, bool tthd, bool flat) {
     switch (op) {
-    case OP_TRANSFER:
-        return tthd ? kvx_copy_kernel<OP_TRANSFER, true> : kvx_copy_kernel<OP_TRANSFER, false>;
-    case OP_GATHER:
-        return tthd ? kvx_copy_kernel<OP_GATHER, true> : kvx_copy_kernel<OP_GATHER, false>;
-    default:
-        return tthd ? kvx_copy_kernel<OP_SCATTER, true> : kvx_copy_kernel<OP_SCATTER, false>;
+    case OP_TRANSFER: return pick_op<OP_TRANSFER>(tthd, flat);
+    case OP_GATHER: return pick_op<OP_GATHER>(tthd, flat);
+    default: return pick_op<OP_SCATTER>(tthd, flat);
     }
 }
 
@@ -413,7 +436,7 @@ KernelFn pick(int op, bool tthd) {
 // Persistent grid: as many workgroups as the device holds at once.
 int launch(const Params &p, hipStream_t stream) {
     const bool tthd = (p.op == OP_GATHER ? p.src : p.dst).tok_contig != 0;
-    KernelFn fn = pick(p.op, tthd);
+    KernelFn fn = pick(p.op, tthd, p.flat != 0);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;

@@ -73,6 +73,15 @@ def test_more_pieces_than_lanes(ls, ld):
                               spec=[(3, 5, 200, None), (0, 0, 128, None), (1, 0, 64, None)]))
 
 
+def test_partial_last_iteration():
+    """A row-resolving tile of 1157 vectors (37 source pages of 32 tokens into
+    one 2048-token page): the last pass of the vector loop covers only part
+    of a wavefront, and those lanes still read page ids held by lanes past
+    the end of the tile."""
+    check(cases.transfer_case("LPCTHD", "LPCTHD", 32, 2048, seed=31, L=2, C=1, H=1, D=8,
+                              spec=[(0, 0, 1157, None), (7, 3, 900, None)]))
+
+
 def test_many_requests_and_empty_ones():
     spec = [((7 * i) % 13, (5 * i) % 11, (i * 37) % 90 if i % 4 else 0, None) for i in range(60)]
     check(cases.transfer_case("LPCTHD", "PLCHTD", 16, 32, seed=5, H=2, D=64, spec=spec))
