@@ -206,6 +206,22 @@ def _len(t) -> int:
     return 0 if t is None else t.numel()
 
 
+def _table(t, name: str):
+    """A page table: a contiguous tensor of 32-bit entries (or None)."""
+    if t is not None and not isinstance(t, int):
+        if t.element_size() != 4 or t.is_floating_point() or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous int32 tensor (got {t.dtype})")
+    return t
+
+
+def _err_word(t):
+    """The optional device error word: one 32-bit integer."""
+    if t is not None and not isinstance(t, int):
+        if t.element_size() != 4 or t.is_floating_point() or t.numel() < 1:
+            raise ValueError(f"dev_err must be a 32-bit integer tensor (got {t.dtype})")
+    return t
+
+
 def _need(t, nbytes: int, name: str) -> None:
     """A tensor argument must hold at least the bytes its descriptor names."""
     if t is None or isinstance(t, int):
@@ -229,6 +245,7 @@ def kvx_transfer(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, dev_err=Non
     _need(src, _pool_nbytes(src_spec), "src")
     _need(dst, _pool_nbytes(dst_spec), "dst")
     S, D = pool_desc(src_spec, src), pool_desc(dst_spec, dst)
+    _table(src_pt, "src_pt"), _table(dst_pt, "dst_pt"), _err_word(dev_err)
     _check(lib().kvx_transfer(ctypes.byref(S), ctypes.byref(D), _ptr(src_pt), _len(src_pt),
                               _ptr(dst_pt), _len(dst_pt), _ptr(reqs), _n_reqs(reqs),
                               _ptr(dev_err), _stream(stream)))
@@ -241,6 +258,7 @@ def kvx_transfer_slice(src, src_spec, dst, dst_spec, sl, src_pt, dst_pt, reqs, d
     _need(src, _pool_nbytes(src_spec), "src")
     _need(dst, _pool_nbytes(dst_spec), "dst")
     S, D, X = pool_desc(src_spec, src), pool_desc(dst_spec, dst), slice_desc(sl)
+    _table(src_pt, "src_pt"), _table(dst_pt, "dst_pt"), _err_word(dev_err)
     _check(lib().kvx_transfer_slice(ctypes.byref(S), ctypes.byref(D), ctypes.byref(X),
                                     _ptr(src_pt), _len(src_pt), _ptr(dst_pt), _len(dst_pt),
                                     _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
@@ -255,6 +273,7 @@ def kvx_transfer_layered(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, lay
     import torch
     _need(src, _pool_nbytes(src_spec), "src")
     _need(dst, _pool_nbytes(dst_spec), "dst")
+    _table(src_pt, "src_pt"), _table(dst_pt, "dst_pt"), _err_word(dev_err)
     st = _stream(stream)
     handles = []
     for ev in events:
@@ -278,6 +297,7 @@ def kvx_gather(src, src_spec, dst, buf_spec, src_pt, reqs, dev_err=None, stream=
     _need(src, _pool_nbytes(src_spec), "src")
     _need(dst, buf_spec.cap * buf_spec.e, "dst")
     S, B = pool_desc(src_spec, src), buf_desc(buf_spec, dst)
+    _table(src_pt, "src_pt"), _err_word(dev_err)
     _check(lib().kvx_gather(ctypes.byref(S), ctypes.byref(B), _ptr(src_pt), _len(src_pt),
                             _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
 
@@ -287,6 +307,7 @@ def kvx_scatter(src, buf_spec, dst, dst_spec, dst_pt, reqs, dev_err=None, stream
     _need(src, buf_spec.cap * buf_spec.e, "src")
     _need(dst, _pool_nbytes(dst_spec), "dst")
     B, D = buf_desc(buf_spec, src), pool_desc(dst_spec, dst)
+    _table(dst_pt, "dst_pt"), _err_word(dev_err)
     _check(lib().kvx_scatter(ctypes.byref(B), ctypes.byref(D), _ptr(dst_pt), _len(dst_pt),
                              _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
 
@@ -315,6 +336,7 @@ def kvx_page_hashes(payload, rec_bytes, page_tokens, reqs, out, dev_err=None, st
         raise ValueError("payload is not a whole number of records")
     if out.element_size() != 8 or not out.is_contiguous() or not payload.is_contiguous():
         raise ValueError("out must be a contiguous 64-bit tensor; payload contiguous")
+    _err_word(dev_err)
     rb = reqs.numel() * reqs.element_size()
     if rb % HASH_REQ_DTYPE.itemsize:
         raise ValueError("reqs must hold whole 32-byte kvx_hash_req records")

@@ -320,3 +320,28 @@ def test_missing_library_raises(monkeypatch, tmp_path):
         kvx.lib()
     with pytest.raises(RuntimeError):
         kvx.kvx_abi_version()
+
+
+def test_binding_rejects_wrong_table_and_error_word_types():
+    """Host-side checks in the binding, before any library call: a page table
+    must be contiguous int32 and the error word one 32-bit integer."""
+    torch = pytest.importorskip("torch")
+    from paper_2606_31093_amd.workloads import PoolSpec
+    P = PoolSpec(1, 1, 1, 8, T=4, N=2, e=2, layout="LPCTHD")
+    a = torch.zeros(P.nbytes, dtype=torch.uint8)
+    reqs = torch.zeros(40, dtype=torch.uint8)
+    t32 = torch.zeros(2, dtype=torch.int32)
+    for bad in (torch.zeros(2, dtype=torch.int64), torch.zeros(2, dtype=torch.float32),
+                torch.zeros(4, dtype=torch.int32)[::2]):
+        with pytest.raises(ValueError, match="int32"):
+            kvx.kvx_transfer(a, P, a, P, bad, t32, reqs)
+        with pytest.raises(ValueError, match="int32"):
+            kvx.kvx_transfer(a, P, a, P, t32, bad, reqs)
+        with pytest.raises(ValueError, match="int32"):
+            kvx.kvx_transfer_slice(a, P, a, P, (0, 0, 1, 0, 0, 1, 0, 0, 1), bad, t32, reqs)
+    with pytest.raises(ValueError, match="dev_err"):
+        kvx.kvx_transfer(a, P, a, P, t32, t32, reqs, dev_err=torch.zeros(1, dtype=torch.int64))
+    with pytest.raises(ValueError, match="dev_err"):
+        kvx.kvx_page_hashes(torch.zeros(16, dtype=torch.uint8), 4, 4,
+                            torch.zeros(32, dtype=torch.uint8), torch.zeros(1, dtype=torch.int64),
+                            dev_err=torch.zeros(1, dtype=torch.float32))
