@@ -92,8 +92,9 @@ int same_shape(const Shape &a, const Shape &b) {
 }
 
 // The device must be able to address `ptr` (device memory or mapped pinned
-// host memory).  On success *dev_ptr is the address kernels use.
-int device_view(const void *ptr, const char *name, void **dev_ptr) {
+// host memory).  On success *dev_ptr is the address kernels use and
+// *is_host (if given) tells whether it is host memory.
+int device_view(const void *ptr, const char *name, void **dev_ptr, bool *is_host = nullptr) {
     hipPointerAttribute_t attr;
     hipError_t e = hipPointerGetAttributes(&attr, ptr);
     if (e != hipSuccess) {
@@ -104,10 +105,12 @@ int device_view(const void *ptr, const char *name, void **dev_ptr) {
     if (attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged ||
         attr.type == hipMemoryTypeUnified) {
         *dev_ptr = const_cast<void *>(ptr);
+        if (is_host) *is_host = false;
         return KVX_OK;
     }
     if (attr.type == hipMemoryTypeHost && attr.devicePointer) {
         *dev_ptr = attr.devicePointer;
+        if (is_host) *is_host = true;
         return KVX_OK;
     }
     return fail(KVX_ERR_RANGE, "%s (%p) is not device memory or mapped pinned host memory", name, ptr);
@@ -206,6 +209,7 @@ int check_common(const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err) {
 // Device views of every pointer a launch uses.
 struct Views {
     void *src = nullptr, *dst = nullptr;
+    bool dst_host = false;
     const int32_t *src_pt = nullptr, *dst_pt = nullptr;
     const kvx_req *reqs = nullptr;
     uint32_t *err = nullptr;
@@ -217,7 +221,7 @@ int view_all(const void *src, const void *dst, const int32_t *src_pt, int64_t sr
     int st;
     void *d = nullptr;
     if ((st = device_view(src, "src base", &v.src))) return st;
-    if ((st = device_view(dst, "dst base", &v.dst))) return st;
+    if ((st = device_view(dst, "dst base", &v.dst, &v.dst_host))) return st;
     if (src_pt_len > 0) {
         if ((st = device_view(src_pt, "src_pt", &d))) return st;
         v.src_pt = static_cast<const int32_t *>(d);
@@ -247,6 +251,7 @@ void finish_params(kvx::Params &P, const Shape &s, const Views &v, int32_t n_req
     P.vpr = P.row_bytes / 16;
     P.elem_bytes = s.e;
     P.flat = P.src.tok_contig && P.dst.tok_contig;
+    P.dst_host = v.dst_host;
     const kvx::Side &ts = P.op == kvx::OP_GATHER ? P.src : P.dst;
     const kvx::Side &os = P.op == kvx::OP_GATHER ? P.dst : P.src;
     P.fd_vpr = kvx::make_fastdiv((uint32_t)P.vpr);

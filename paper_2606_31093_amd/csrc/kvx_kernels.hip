@@ -82,12 +82,17 @@ __device__ __forceinline__ v4u ld16(const char *p) {
 #endif
 }
 
+// Stores into device memory stream past the caches; stores into pinned host
+// memory (HOST) are ordinary, which measured faster over PCIe.
+template <bool HOST>
 __device__ __forceinline__ void st16(char *p, v4u v) {
 #if KVX_NT_STORE
-    __builtin_nontemporal_store(v, reinterpret_cast<v4u *>(p));
-#else
-    *reinterpret_cast<v4u *>(p) = v;
+    if (!HOST) {
+        __builtin_nontemporal_store(v, reinterpret_cast<v4u *>(p));
+        return;
+    }
 #endif
+    *reinterpret_cast<v4u *>(p) = v;
 }
 
 __device__ __forceinline__ void report(const Params &p, uint32_t bits) {
@@ -145,7 +150,7 @@ __device__ __forceinline__ bool load_req(const Params &p, int32_t r, Req &q) {
 }
 
 // Plain vector stream over C runs of R vectors each, by a worker of NT threads.
-template <int NT, int U>
+template <int NT, int U, bool HOST>
 __device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, int64_t s_sc,
                                           uint32_t R, int32_t C) {
     const uint32_t total = R * (uint32_t)C;
@@ -166,7 +171,7 @@ __device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, 
             if (k < total) {
                 const uint32_t c = k >= R;
                 const uint32_t w = k - c * R;
-                st16(d + c * d_sc + (int64_t)w * 16, v[u]);
+                st16<HOST>(d + c * d_sc + (int64_t)w * 16, v[u]);
             }
         }
     }
@@ -190,7 +195,7 @@ struct Tile {
 // General row-resolving copy.  Vectors are enumerated in the tiling side's
 // memory order: (c, slot, h, v) when it is token-major, else (c, h, slot, v)
 // over whole pages with the slots outside [sa, sb) masked.
-template <int OP, bool TTHD, int NT, int U>
+template <int OP, bool TTHD, int NT, bool HOST, int U>
 __device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const Tile &t) {
     constexpr bool kTileSrc = OP == OP_GATHER;
     constexpr bool kOtherBuf = OP != OP_TRANSFER;
@@ -263,11 +268,11 @@ __device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const T
             if (ok[u]) val[u] = ld16(src[u]);
 #pragma unroll
         for (int u = 0; u < U; ++u)
-            if (ok[u]) st16(dst[u], val[u]);
+            if (ok[u]) st16<HOST>(dst[u], val[u]);
     }
 }
 
-template <int OP, bool TTHD, int NT>
+template <int OP, bool TTHD, int NT, bool HOST>
 __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t local) {
     constexpr bool kTileSrc = OP == OP_GATHER;
     constexpr bool kOtherBuf = OP != OP_TRANSFER;
@@ -311,10 +316,10 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
         if (p.flat) {
             const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
             if (kTileSrc)
-                copy_runs<NT, KVX_UNROLL_FLAT>(const_cast<char *>(t.o_row0), tb, t.o_sc, ts.s_c,
+                copy_runs<NT, KVX_UNROLL_FLAT, HOST>(const_cast<char *>(t.o_row0), tb, t.o_sc, ts.s_c,
                                            (uint32_t)run_t, p.C);
             else
-                copy_runs<NT, KVX_UNROLL_FLAT>(const_cast<char *>(tb), t.o_row0, ts.s_c, t.o_sc,
+                copy_runs<NT, KVX_UNROLL_FLAT, HOST>(const_cast<char *>(tb), t.o_row0, ts.s_c, t.o_sc,
                                            (uint32_t)run_t, p.C);
             return;
         }
@@ -345,12 +350,12 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
             const char *ob = os.base + (int64_t)t.l * os.s_l + (int64_t)pg * os.s_p +
                              (int64_t)so0 * os.s_t;
             const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
-            copy_runs<NT, KVX_UNROLL_FLAT>(const_cast<char *>(tb), ob, ts.s_c, os.s_c,
+            copy_runs<NT, KVX_UNROLL_FLAT, HOST>(const_cast<char *>(tb), ob, ts.s_c, os.s_c,
                                        (uint32_t)run_t, p.C);
             return;
         }
     }
-    copy_rows<OP, TTHD, NT, KVX_UNROLL_ROWS>(p, q, t);
+    copy_rows<OP, TTHD, NT, HOST, KVX_UNROLL_ROWS>(p, q, t);
 }
 
 // Inclusive sum of x over the workgroup's threads (x = 0 past the chunk).
@@ -368,7 +373,7 @@ __device__ __forceinline__ int64_t block_scan(int64_t x, int64_t *s_wave) {
     return x;
 }
 
-template <int OP, bool TTHD, int NT>
+template <int OP, bool TTHD, int NT, bool HOST>
 __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
     constexpr int kWorkers = kBlock / NT;
     // Records are taken kBlock at a time: each thread reads one and counts
@@ -404,7 +409,7 @@ __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
                 load_req<OP>(p, r0 + lo, q);
                 cached = r0 + lo;
             }
-            do_tile<OP, TTHD, NT>(p, q, local - (lo ? s_end[lo - 1] : 0));
+            do_tile<OP, TTHD, NT, HOST>(p, q, local - (lo ? s_end[lo - 1] : 0));
         }
         chunk_base += chunk_tiles;
         __syncthreads();                             // s_end and s_wave are rewritten next chunk
@@ -416,18 +421,22 @@ typedef void (*KernelFn)(Params);
 constexpr int kFlatNT = KVX_FLAT_WAVE_TILES ? kWave : kBlock;
 constexpr int kRowsNT = KVX_ROWS_WAVE_TILES ? kWave : kBlock;
 
-template <int OP>
+template <int OP, bool HOST>
 KernelFn pick_op(bool tthd, bool flat) {
     if (flat)
-        return tthd ? kvx_copy_kernel<OP, true, kFlatNT> : kvx_copy_kernel<OP, false, kFlatNT>;
-    return tthd ? kvx_copy_kernel<OP, true, kRowsNT> : kvx_copy_kernel<OP, false, kRowsNT>;
+        return tthd ? kvx_copy_kernel<OP, true, kFlatNT, HOST>
+                    : kvx_copy_kernel<OP, false, kFlatNT, HOST>;
+    return tthd ? kvx_copy_kernel<OP, true, kRowsNT, HOST> : kvx_copy_kernel<OP, false, kRowsNT, HOST>;
 }
 
-KernelFn pick(int op, bool tthd, bool flat) {
+KernelFn pick(int op, bool tthd, bool flat, bool host) {
     switch (op) {
-    case OP_TRANSFER: return pick_op<OP_TRANSFER>(tthd, flat);
-    case OP_GATHER: return pick_op<OP_GATHER>(tthd, flat);
-    default: return pick_op<OP_SCATTER>(tthd, flat);
+    case OP_TRANSFER:
+        return host ? pick_op<OP_TRANSFER, true>(tthd, flat) : pick_op<OP_TRANSFER, false>(tthd, flat);
+    case OP_GATHER:
+        return host ? pick_op<OP_GATHER, true>(tthd, flat) : pick_op<OP_GATHER, false>(tthd, flat);
+    default:
+        return host ? pick_op<OP_SCATTER, true>(tthd, flat) : pick_op<OP_SCATTER, false>(tthd, flat);
     }
 }
 
@@ -436,7 +445,7 @@ KernelFn pick(int op, bool tthd, bool flat) {
 // Persistent grid: as many workgroups as the device holds at once.
 int launch(const Params &p, hipStream_t stream) {
     const bool tthd = (p.op == OP_GATHER ? p.src : p.dst).tok_contig != 0;
-    KernelFn fn = pick(p.op, tthd, p.flat != 0);
+    KernelFn fn = pick(p.op, tthd, p.flat != 0, p.dst_host != 0);
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
