@@ -27,8 +27,7 @@
  * - The caller owns every buffer, table, record array, error word and
  *   stream.
  * - The library allocates no device or host memory and keeps no state
- *   between calls.  It keeps a thread-local error message and a per-device
- *   launch-shape cache.
+ *   between calls other than a thread-local error message.
  * - Page tables, request records and the error word must be readable and
  *   writable by the device: device memory, or pinned host memory mapped for
  *   the device.
@@ -71,7 +70,8 @@ extern "C" {
 
 #define KVX_ABI_VERSION 1
 
-/* Most request records per call (each workgroup walks the record array). */
+/* Most request records per call (each workgroup of the copy kernel reads
+ * the whole record array, 256 records at a time). */
 #define KVX_MAX_REQS 65536
 /* Largest page (tokens) a pool may declare. */
 #define KVX_MAX_PAGE_TOKENS (1 << 20)
@@ -106,7 +106,8 @@ typedef enum kvx_status {
 #define KVX_DERR_BAD_REQ 8u
 
 /* A paged pool of num_pages pages; element (l, p, c, t, h, d) lives where
- * `layout` puts it.  `base` is device memory, 16-byte aligned. */
+ * `layout` puts it.  `base` is device memory (or device-mapped pinned host
+ * memory), 16-byte aligned. */
 typedef struct kvx_pool {
     void *base;
     int32_t num_layers;  /* L >= 1 */
