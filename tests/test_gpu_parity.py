@@ -64,6 +64,25 @@ def test_gather_scatter(layout, T, e, D, pinned):
     check(cases.gather_scatter_case(layout, T, e, D, seed=T * 31 + e * 7 + D, pinned=pinned))
 
 
+@pytest.mark.parametrize("ls,ld,Ts,Td", [("LPCTHD", "LPCTHD", 16, 16), ("LPCTHD", "LPCTHD", 4, 16),
+                                         ("LPCTHD", "PLCHTD", 16, 64), ("PLCHTD", "LPCHTD", 8, 4)])
+def test_transfer_into_pinned_host_pool(ls, ld, Ts, Td):
+    """A destination pool in pinned host memory (ordinary stores over PCIe),
+    on contiguous-run and row-resolving launches."""
+    wl = cases.transfer_case(ls, ld, Ts, Td, seed=Ts * 13 + Td)
+    wl.host_sides = ("B",)
+    check(wl)
+
+
+@pytest.mark.parametrize("layout", ["LPCTHD", "PLCHTD"])
+def test_scatter_into_pinned_host_pool(layout):
+    """Gather into a pinned host buffer, then scatter from it into a pool that
+    is also pinned host memory."""
+    wl = cases.gather_scatter_case(layout, 16, 2, 64, seed=41, pinned=True)
+    wl.host_sides = ("buf", "B")
+    check(wl)
+
+
 @pytest.mark.parametrize("ls,ld", [("LPCTHD", "LPCTHD"), ("LPCTHD", "PLCHTD"),
                                    ("PLCHTD", "LPCHTD")])
 def test_more_pieces_than_lanes(ls, ld):
