@@ -252,11 +252,9 @@ void finish_params(kvx::Params &P, const Shape &s, const Views &v, int32_t n_req
     P.elem_bytes = s.e;
     P.flat = P.src.tok_contig && P.dst.tok_contig;
     P.dst_host = v.dst_host;
-    const kvx::Side &ts = P.op == kvx::OP_GATHER ? P.src : P.dst;
     const kvx::Side &os = P.op == kvx::OP_GATHER ? P.dst : P.src;
     P.fd_vpr = kvx::make_fastdiv((uint32_t)P.vpr);
     P.fd_H = kvx::make_fastdiv((uint32_t)P.H);
-    P.fd_Tt = kvx::make_fastdiv((uint32_t)ts.T);
     P.fd_To = kvx::make_fastdiv((uint32_t)os.T);
 }
 

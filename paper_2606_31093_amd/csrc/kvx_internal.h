@@ -67,7 +67,7 @@ struct Params {
     int32_t elem_bytes;
     int32_t flat;        // both sides tok_contig: a tile is C contiguous runs per piece
     int32_t dst_host;    // the destination is pinned host memory (plain stores)
-    FastDiv fd_vpr, fd_H, fd_Tt, fd_To;
+    FastDiv fd_vpr, fd_H, fd_To;
 };
 
 // Launch on `stream`; returns a hipError_t value.
