@@ -264,6 +264,10 @@ uint32_t ora_transfer_slice(const uint8_t *src, const ora_pool *S, uint8_t *dst,
                             const int64_t *reqs, int64_t n_reqs)
 {
     uint32_t err = 0;
+    /* A slice with no layer, kv component or head copies no element, and a
+     * call that copies nothing checks nothing: no record or table is read. */
+    if (sl[2] == 0 || sl[5] == 0 || sl[8] == 0)
+        return 0;
     for (int64_t r = 0; r < n_reqs; ++r) {
         const int64_t *q = reqs + 6 * r;
         int64_t n = q[R_N];

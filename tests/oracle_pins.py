@@ -583,6 +583,13 @@ def pin_slice_errors(O):
         assert O.transfer_slice(src, S, d, Dp, sl, spt, dpt, [row]) == bits, (spt, dpt, row)
         if bits == ERR_DST_PAGE or bits == ERR_BAD_REQ:
             _same(d, base, "skipped positions written")
+    # a slice with no layer, kv component or head copies nothing and checks
+    # nothing: damaged tables and malformed records raise no bit
+    for empty in ((1, 0, 0, 1, 0, 1, 0, 0, 2), (1, 0, 1, 1, 0, 0, 0, 0, 2),
+                  (1, 0, 1, 1, 0, 1, 0, 0, 0)):
+        d = base.copy()
+        assert O.transfer_slice(src, S, d, Dp, empty, [9, 9], [-1, 7], [_req(n=8), _req(n=-2)]) == 0
+        _same(d, base, "an empty slice wrote")
 
 
 

@@ -82,6 +82,7 @@ MUTANTS = {
     "slice_src_kv_offset_dropped": ("sl[3] + c", "c"),
     "slice_one_layer_short": ("l < sl[2]", "l + 1 < sl[2]"),
     "slice_heads_of_the_pool": ("h < sl[8]", "h < S->H"),
+    "empty_slice_checked": ("    if (sl[2] == 0 || sl[5] == 0 || sl[8] == 0)\n        return 0;\n", ""),
     "fnv1_instead_of_fnv1a": ("        h ^= p[i];\n        h *= FNV_PRIME;",
                               "        h *= FNV_PRIME;\n        h ^= p[i];"),
     "chain_pair_swapped": ("le64(pair, h);\n            le64(pair + 8, c);",
