@@ -115,3 +115,68 @@ SLICES = [((4, 2, 8), (2, 2, 4), (2, 0, 2, 0, 0, 2, 4, 0, 4)),     # TP=2 shard 
           ((2, 1, 1), (2, 1, 3), (0, 0, 2, 0, 0, 1, 0, 2, 1)),     # one head into head 2
           ((2, 2, 4), (2, 2, 4), (0, 0, 2, 0, 0, 2, 0, 0, 4)),     # everything
           ((2, 2, 8), (2, 2, 8), (1, 0, 1, 1, 0, 1, 3, 5, 1))]     # one row per token
+
+
+def random_case(seed: int) -> Workload:
+    """A seeded random pool -> pool case: layouts, page sizes (powers of two
+    and not), shapes, element widths, 1-6 requests with random starts and
+    lengths (some empty, some rereading an earlier request's source pages),
+    sometimes a slice with its own layer/kv/head ranges, and sometimes one
+    damaged page-table entry or a truncated table.  Destinations never
+    overlap, so the result is defined even with the damage."""
+    rng = np.random.default_rng(10_000 + seed)
+    pick = lambda xs: xs[int(rng.integers(len(xs)))]
+    ls, ld = pick(LAYOUTS), pick(LAYOUTS)
+    Ts, Td = pick([1, 2, 3, 4, 5, 8, 16, 32, 64]), pick([1, 2, 3, 4, 6, 8, 16, 32, 64])
+    e = pick([1, 2, 4, 8])
+    D = (16 // e) * pick([1, 2, 3, 5])
+    sliced = rng.random() < 0.3
+    if sliced:
+        Ls, Ld = int(rng.integers(1, 4)), int(rng.integers(1, 4))
+        Cs, Cd = int(rng.integers(1, 3)), int(rng.integers(1, 3))
+        Hs, Hd = pick([1, 2, 3, 5]), pick([1, 2, 3, 5])
+        ranges = []
+        for a, b in ((Ls, Ld), (Cs, Cd), (Hs, Hd)):
+            n = int(rng.integers(0 if rng.random() < 0.1 else 1, min(a, b) + 1))
+            ranges.append((int(rng.integers(0, a - n + 1)), int(rng.integers(0, b - n + 1)), n))
+        sl = tuple(x for r in ranges for x in r)
+    else:
+        Ls = Ld = int(rng.integers(1, 4))
+        Cs = Cd = int(rng.integers(1, 3))
+        Hs = Hd = pick([1, 2, 3, 5])
+        sl = None
+    spec = []
+    for r in range(int(rng.integers(1, 7))):
+        n = 0 if rng.random() < 0.1 else int(rng.integers(1, 3 * max(Ts, Td) + 6))
+        share = int(rng.integers(0, r)) if r and rng.random() < 0.2 else None
+        spec.append((int(rng.integers(0, 2 * Ts)), int(rng.integers(0, 2 * Td)), n, share))
+    ks = [_cdiv(s0 + n, Ts) for s0, _d0, n, share in spec if share is None]
+    kd = [_cdiv(d0 + n, Td) for _s0, d0, n, _share in spec]
+    S = PoolSpec(Ls, Cs, Hs, D, T=Ts, N=sum(ks) + 2, e=e, layout=ls)
+    Dp = PoolSpec(Ld, Cd, Hd, D, T=Td, N=sum(kd) + 2, e=e, layout=ld)
+    sperm, dperm = rng.permutation(S.N).astype(np.int32), rng.permutation(Dp.N).astype(np.int32)
+    src_pt, dst_pt, rows, src_offs = [], [], [], []
+    for s0, d0, n, share in spec:
+        k_s, k_d = _cdiv(s0 + n, Ts), _cdiv(d0 + n, Td)
+        so = src_offs[share] if share is not None else len(src_pt)
+        if share is None:
+            src_pt.extend(sperm[len(src_pt): len(src_pt) + k_s])
+        src_offs.append(so)
+        rows.append([so, len(dst_pt), 0, s0, d0, n])
+        dst_pt.extend(dperm[len(dst_pt): len(dst_pt) + k_d])
+    src_pt, dst_pt = np.asarray(src_pt, np.int32), np.asarray(dst_pt, np.int32)
+    damage = rng.random()
+    if damage < 0.08 and len(dst_pt):
+        dst_pt[int(rng.integers(len(dst_pt)))] = pick([-1, Dp.N, 2**31 - 1])
+    elif damage < 0.16 and len(src_pt):
+        src_pt[int(rng.integers(len(src_pt)))] = pick([-1, S.N])
+    elif damage < 0.22 and len(src_pt) > 1:
+        src_pt = src_pt[: int(rng.integers(1, len(src_pt)))]
+    step = Step("transfer", "A", "B", src_pt, dst_pt, np.asarray(rows, np.int64).reshape(-1, 6),
+                slice=sl)
+    return Workload("case", f"random {seed}: {ls}/T{Ts} ({Ls},{Cs},{Hs}) -> {ld}/T{Td} "
+                    f"({Ld},{Cd},{Hd}) e{e} D{D} slice={sl}",
+                    {"A": S, "B": Dp}, [step], value_seed=seed, prefill_tag=seed & 0xFF)
+
+
+RANDOM_CASES = 200

@@ -101,6 +101,13 @@ def test_partial_last_iteration():
                               spec=[(0, 0, 1157, None), (7, 3, 900, None)]))
 
 
+@pytest.mark.parametrize("seed", range(cases.RANDOM_CASES))
+def test_random_cases(seed):
+    """Seeded random pool -> pool cases (layouts, page sizes, shapes, element
+    widths, ranges, shared pages, slices, damaged tables)."""
+    check(cases.random_case(seed))
+
+
 def test_many_requests_and_empty_ones():
     spec = [((7 * i) % 13, (5 * i) % 11, (i * 37) % 90 if i % 4 else 0, None) for i in range(60)]
     check(cases.transfer_case("LPCTHD", "PLCHTD", 16, 32, seed=5, H=2, D=64, spec=spec))

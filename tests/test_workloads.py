@@ -111,3 +111,32 @@ def test_bf16_rounding_nearest_even():
     # values decode to roughly N(0, 1)
     f = (x.astype(np.uint32) << 16).view(np.float32)
     assert abs(float(f.mean())) < 0.1 and 0.9 < float(f.std()) < 1.1
+
+
+def test_random_cases_are_well_formed():
+    """The seeded random parity cases: destination pages disjoint across
+    requests, slice ranges inside both pools, and the oracle runs each one
+    (some raise device bits by design)."""
+    import sys, os
+    sys.path.insert(0, os.path.dirname(__file__))
+    import cases
+    from runner import initial_bytes, run_oracle
+    bits = set()
+    for seed in range(cases.RANDOM_CASES):
+        wl = cases.random_case(seed)
+        st = wl.steps[0]
+        S, D = wl.sides["A"], wl.sides["B"]
+        used = []
+        for so, do, bo, s0, d0, n in st.reqs:
+            if n:
+                used.extend(range(do + d0 // D.T, do + (d0 + n - 1) // D.T + 1))
+        assert len(used) == len(set(used))
+        if st.slice is not None:
+            sl = st.slice
+            for a0, b0, cnt, amax, bmax in ((sl[0], sl[1], sl[2], S.L, D.L),
+                                            (sl[3], sl[4], sl[5], S.C, D.C),
+                                            (sl[6], sl[7], sl[8], S.H, D.H)):
+                assert a0 + cnt <= amax and b0 + cnt <= bmax
+        _, errs = run_oracle(wl, initial_bytes(wl))
+        bits.add(errs[0])
+    assert 0 in bits and len(bits) > 2
