@@ -180,3 +180,60 @@ def random_case(seed: int) -> Workload:
 
 
 RANDOM_CASES = 200
+
+
+def random_gs_case(seed: int) -> Workload:
+    """A seeded random gather (pool -> flat buffer) and scatter (buffer ->
+    a second pool): random layout, page size, shape and element width, 1-5
+    requests at random source / destination starts, blocks at random aligned
+    offsets with gaps, the buffer in device or pinned host memory, and
+    sometimes a damaged record (a block that is misaligned or runs past the
+    buffer, a nonzero buffer-side start) or a damaged page id."""
+    rng = np.random.default_rng(20_000 + seed)
+    pick = lambda xs: xs[int(rng.integers(len(xs)))]
+    layout, T = pick(LAYOUTS), pick([1, 2, 3, 4, 8, 16, 64])
+    e = pick([1, 2, 4, 8])
+    D = (16 // e) * pick([1, 2, 3])
+    L, C, H = int(rng.integers(1, 4)), int(rng.integers(1, 3)), pick([1, 2, 3])
+    align = 16 // e
+    ns = [0 if rng.random() < 0.1 else int(rng.integers(1, 3 * T + 6))
+          for _ in range(int(rng.integers(1, 6)))]
+    starts = [int(rng.integers(0, 2 * T)) for _ in ns]
+    dstarts = [int(rng.integers(0, 2 * T)) for _ in ns]
+    blocks, off = [], int(rng.integers(0, 3)) * align
+    for n in ns:
+        blocks.append(off)
+        off += _cdiv(L * C * n * H * D, align) * align + int(rng.integers(0, 3)) * align
+    B = BufSpec(L, C, H, D, e, cap=off)
+    S = PoolSpec(L, C, H, D, T=T, N=sum(_cdiv(s + n, T) for n, s in zip(ns, starts)) + 2, e=e,
+                 layout=layout)
+    P2 = PoolSpec(L, C, H, D, T=T, N=sum(_cdiv(s + n, T) for n, s in zip(ns, dstarts)) + 2, e=e,
+                  layout=layout)
+    perm, dperm = rng.permutation(S.N).astype(np.int32), rng.permutation(P2.N).astype(np.int32)
+    g_rows, s_rows, pt, dpt = [], [], [], []
+    for n, s0, d0, bo in zip(ns, starts, dstarts, blocks):
+        g_rows.append([len(pt), 0, bo, s0, 0, n])
+        s_rows.append([0, len(dpt), bo, 0, d0, n])
+        pt.extend(perm[len(pt): len(pt) + _cdiv(s0 + n, T)])
+        dpt.extend(dperm[len(dpt): len(dpt) + _cdiv(d0 + n, T)])
+    g_rows, s_rows = np.asarray(g_rows, np.int64), np.asarray(s_rows, np.int64)
+    pt, dpt = np.asarray(pt, np.int32), np.asarray(dpt, np.int32)
+    damage, r = rng.random(), int(rng.integers(len(ns)))
+    if damage < 0.05 and e < 8:
+        g_rows[r, 2] += 1                      # block not 16-byte aligned
+    elif damage < 0.10:
+        s_rows[r, 2] = off                     # block runs past the buffer (if n > 0)
+    elif damage < 0.14:
+        g_rows[r, 4] = 1                       # buffer-side start must be 0
+    elif damage < 0.20 and len(pt):
+        pt[int(rng.integers(len(pt)))] = S.N
+    elif damage < 0.26 and len(dpt):
+        dpt[int(rng.integers(len(dpt)))] = -1
+    steps = [Step("gather", "A", "buf", pt, None, g_rows),
+             Step("scatter", "buf", "B", None, dpt, s_rows)]
+    return Workload("case", f"random gather/scatter {seed}: {layout}/T{T} ({L},{C},{H}) e{e} D{D}",
+                    {"A": S, "buf": B, "B": P2}, steps, value_seed=seed, prefill_tag=seed & 0xFF,
+                    host_sides=("buf",) if rng.random() < 0.3 else ())
+
+
+RANDOM_GS_CASES = 100

@@ -108,6 +108,13 @@ def test_random_cases(seed):
     check(cases.random_case(seed))
 
 
+@pytest.mark.parametrize("seed", range(cases.RANDOM_GS_CASES))
+def test_random_gather_scatter(seed):
+    """Seeded random gathers into a flat buffer (device or pinned host) and
+    scatters back into a second pool, with damaged records and page ids."""
+    check(cases.random_gs_case(seed))
+
+
 def test_many_requests_and_empty_ones():
     spec = [((7 * i) % 13, (5 * i) % 11, (i * 37) % 90 if i % 4 else 0, None) for i in range(60)]
     check(cases.transfer_case("LPCTHD", "PLCHTD", 16, 32, seed=5, H=2, D=64, spec=spec))

@@ -140,3 +140,12 @@ def test_random_cases_are_well_formed():
         _, errs = run_oracle(wl, initial_bytes(wl))
         bits.add(errs[0])
     assert 0 in bits and len(bits) > 2
+    gs_bits = set()
+    for seed in range(cases.RANDOM_GS_CASES):
+        wl = cases.random_gs_case(seed)
+        B = wl.sides["buf"]
+        for so, do, bo, s0, d0, n in wl.steps[0].reqs:
+            assert bo >= 0
+        _, errs = run_oracle(wl, initial_bytes(wl))
+        gs_bits.add(tuple(errs))
+    assert (0, 0) in gs_bits and len(gs_bits) > 2
