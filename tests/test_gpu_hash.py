@@ -104,3 +104,34 @@ def test_chain_lengths_and_scattered_outputs(torch):
     got, gerr, want, werr = _both(torch, pay, 4, T, rows, cursor + 7)
     assert gerr == werr == 0
     assert np.array_equal(got, want)
+
+
+def _random_hash_case(seed):
+    rng = np.random.default_rng(30_000 + seed)
+    rec_bytes = int(rng.choice([4, 8, 12, 16, 40]))
+    T = int(rng.choice([1, 2, 3, 7, 16, 64, 100]))
+    nreq = int(rng.integers(1, 40))
+    n = [0 if rng.random() < 0.1 else int(rng.integers(1, 6 * T + 10)) for _ in range(nreq)]
+    positions = max(1, sum(n) // 2 + max(n))
+    rows, out = [], int(rng.integers(0, 4))
+    for k in n:
+        off = int(rng.integers(0, positions - k + 1))      # payload ranges may overlap
+        seed_v = int(rng.integers(0, 2**63)) if rng.random() < 0.4 else 0
+        rows.append((off, out, seed_v, k))
+        out += -(-k // T) + int(rng.integers(0, 3))
+    out_len = out + int(rng.integers(0, 3))
+    if rng.random() < 0.2:                                   # a malformed record
+        r = int(rng.integers(nreq))
+        po, oo, sv, k = rows[r]
+        rows[r] = rng.choice([(po, oo, sv, -1), (positions, oo, sv, k + 1), (po, out_len, sv, k + T)])
+        rows[r] = tuple(int(x) for x in rows[r])
+    pay = rng.integers(0, 2**31, size=positions * rec_bytes // 4, dtype=np.int32)
+    return pay, rec_bytes, T, rows, out_len
+
+
+@pytest.mark.parametrize("seed", range(50))
+def test_random_hash_cases(torch, seed):
+    pay, rec_bytes, T, rows, out_len = _random_hash_case(seed)
+    got, gerr, want, werr = _both(torch, pay, rec_bytes, T, rows, out_len)
+    assert gerr == werr
+    assert np.array_equal(got, want)
