@@ -74,6 +74,39 @@ def test_transfer_into_pinned_host_pool(ls, ld, Ts, Td):
     check(wl)
 
 
+def test_offset_views_into_pinned_host_memory():
+    """A flat buffer and a pool that start inside larger pinned allocations
+    (16-byte aligned views at an offset): the device addresses the library
+    derives must keep the offset."""
+    import torch
+    from paper_2606_31093_amd import kvx
+    wl = cases.gather_scatter_case("LPCTHD", 16, 2, 64, seed=57)
+    g, sc = wl.steps
+    A, B, P2 = wl.sides["A"], wl.sides["buf"], wl.sides["B"]
+    init = initial_bytes(wl)
+    want, werr = run_oracle(wl, init)
+    pad = 4096 + 48
+    hbuf = torch.zeros(B.nbytes + 2 * pad, dtype=torch.uint8, pin_memory=True)
+    hpool = torch.zeros(P2.nbytes + 2 * pad, dtype=torch.uint8, pin_memory=True)
+    hbuf.fill_(0xA5)
+    hpool.fill_(0xA5)
+    buf = hbuf[pad:pad + B.nbytes]
+    pool = hpool[pad:pad + P2.nbytes]
+    buf.copy_(torch.from_numpy(init["buf"]))
+    pool.copy_(torch.from_numpy(init["B"]))
+    src = torch.from_numpy(init["A"]).cuda()
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kvx.kvx_gather(src, A, buf, B, kvx.device_table(g.src_pt), kvx.device_reqs(g.reqs), err)
+    kvx.kvx_scatter(buf, B, pool, P2, kvx.device_table(sc.dst_pt), kvx.device_reqs(sc.reqs), err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0 and werr == [0, 0]
+    assert np.array_equal(buf.numpy(), want["buf"])
+    assert np.array_equal(pool.numpy(), want["B"])
+    for whole in (hbuf, hpool):                       # nothing outside the views
+        h = whole.numpy()
+        assert (h[:pad] == 0xA5).all() and (h[-pad:] == 0xA5).all()
+
+
 @pytest.mark.parametrize("layout", ["LPCTHD", "PLCHTD"])
 def test_scatter_into_pinned_host_pool(layout):
     """Gather into a pinned host buffer, then scatter from it into a pool that
