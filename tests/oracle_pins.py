@@ -22,6 +22,7 @@ The pins:
 from __future__ import annotations
 
 import itertools
+import json
 import os
 import sys
 
@@ -58,6 +59,27 @@ def _same(a, b, what):
 # worked examples written out by hand
 # ---------------------------------------------------------------------------
 
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden_rows(name: str) -> list:
+    """Tab-separated rows of a fixture under tests/golden (comments skipped)."""
+    rows = []
+    with open(os.path.join(GOLDEN, name)) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                rows.append(line.rstrip("\n").split("\t"))
+    return rows
+
+
+def _check_golden_example(example: str, dst: np.ndarray) -> None:
+    rows = [r for r in _golden_rows("layout_hand_examples.txt") if r[0] == example]
+    assert rows, example
+    for _, start, count, value in rows:
+        a, n = int(start), int(count)
+        assert (dst[a:a + n] == int(value)).all(), (example, a, n, value, dst[a:a + n])
+
+
 def pin_hand_example(O):
     """One head of 8 bf16 per row.  Source: 4 pages x 2 tokens, page p slot s
     holds the row filled with 10p + s.  Request: source table [3, 1], start
@@ -75,9 +97,7 @@ def pin_hand_example(O):
     err = O.transfer(src.reshape(-1).view(np.uint8), S, dst.reshape(-1).view(np.uint8), Dp,
                      [3, 1], [1], [_req(s0=1, d0=0, n=3)])
     assert err == 0, err
-    assert (dst[0] == 999).all(), dst[0]
-    assert [int(dst[1, s, 0]) for s in range(4)] == [31, 10, 11, 999], dst[1, :, 0]
-    assert (dst[1] == dst[1, :, :1]).all()
+    _check_golden_example("lpcthd", dst.reshape(-1))
 
 
 def pin_hand_example_plchtd(O):
@@ -101,13 +121,7 @@ def pin_hand_example_plchtd(O):
     err = O.transfer(src.reshape(-1).view(np.uint8), S, dst.view(np.uint8), Dp,
                      [2, 0], [1], [_req(s0=0, d0=1, n=3)])
     assert err == 0, err
-    assert (dst[440:448] == 1010).all(), dst[440:448]
-    assert (dst[328:336] == 108).all(), dst[328:336]
-    # page 1, layer 0, kv 0, head 0: slots 0..3 start at element
-    # (((1*2+0)*2+0)*2+0)*4*8 = 256 and hold untouched, 8, 9, 0
-    assert list(dst[256:288:8]) == [7, 8, 9, 0], dst[256:288:8]
-    # destination page 0 untouched
-    assert (dst[: 2 * 2 * 2 * 4 * 8] == 7).all()
+    _check_golden_example("plchtd", dst)
 
 
 # ---------------------------------------------------------------------------
@@ -632,10 +646,13 @@ FNV_BASIS = 0xcbf29ce484222325
 
 
 def pin_fnv_published_vectors(O):
-    """FNV-1a 64 test vectors published with the algorithm."""
-    for data, want in ((b"", 0xcbf29ce484222325), (b"a", 0xaf63dc4c8601ec8c),
-                       (b"foobar", 0x85944171f73967e8)):
-        assert O.fnv1a64(data) == want, (data, hex(O.fnv1a64(data)))
+    """FNV-1a 64 test vectors published with the algorithm
+    (tests/golden/fnv1a64_vectors.txt)."""
+    rows = _golden_rows("fnv1a64_vectors.txt")
+    assert len(rows) >= 3
+    for text, want in rows:
+        data = json.loads(text).encode("ascii")
+        assert O.fnv1a64(data) == int(want, 16), (data, hex(O.fnv1a64(data)))
 
 
 def _hashes(O, payload, rec_bytes, T, rows, n_out):
