@@ -301,6 +301,93 @@ uint32_t ora_transfer_slice(const uint8_t *src, const ora_pool *S, uint8_t *dst,
     return err;
 }
 
+/* Slice of a pool -> flat buffer (Sec. 4.1.2 migration restricted to a
+ * view, Sec. 4.1.1: a view names a tuple of layers and a tuple of slices).
+ * sl is the nine-field slice of ora_transfer_slice.  Write (L0, K0, H0)
+ * for its source offsets (fields 0, 3, 6) and (nl, nk, nh) for its counts
+ * (fields 2, 5, 8).  The buffer holds exactly the slice: its blocks are
+ * [nl][nk][n][nh][D] (the buffer shape's L, C, H).  For every request r,
+ * token i < n, layer l < nl, kv c < nk, head h < nh and every d:
+ *     block_r(l, c, i, h, d) := POOL(L0 + l, K0 + c, src_start + i, H0 + h, d)
+ * A slice with a zero count copies and checks nothing. */
+uint32_t ora_gather_slice(const uint8_t *src, const ora_pool *S, uint8_t *dst,
+                          const ora_buf *B, const int64_t *sl,
+                          const int32_t *src_pt, int64_t src_pt_len,
+                          const int64_t *reqs, int64_t n_reqs)
+{
+    uint32_t err = 0;
+    if (sl[2] == 0 || sl[5] == 0 || sl[8] == 0)
+        return 0;
+    for (int64_t r = 0; r < n_reqs; ++r) {
+        const int64_t *q = reqs + 6 * r;
+        int64_t n = q[R_N];
+        if (!range_ok(q[R_SRC_START], n) || q[R_DST_START] != 0 ||
+            !block_ok(B, q[R_BUF], n)) {
+            err |= ORA_ERR_BAD_REQ;
+            continue;
+        }
+        for (int64_t i = 0; i < n; ++i) {
+            int64_t sp, ss;
+            int bad = resolve(S, src_pt, src_pt_len, q[R_SRC_PT],
+                              q[R_SRC_START] + i, ORA_ERR_SRC_PAGE, &sp, &ss);
+            if (bad) {
+                err |= (uint32_t)bad;
+                continue;
+            }
+            for (int64_t l = 0; l < sl[2]; ++l)
+                for (int64_t c = 0; c < sl[5]; ++c)
+                    for (int64_t h = 0; h < sl[8]; ++h)
+                        for (int64_t d = 0; d < S->D; ++d)
+                            copy_elem(dst + B->e * buf_index(B, q[R_BUF], n, l, c, i, h, d),
+                                      src + S->e * pool_index(S, sl[0] + l, sl[3] + c,
+                                                              sp, ss, sl[6] + h, d),
+                                      S->e);
+        }
+    }
+    return err;
+}
+
+/* Flat buffer -> slice of a pool: the reverse of ora_gather_slice, with
+ * the pool's range starting at the slice's destination offsets (L1, K1, H1)
+ * (fields 1, 4, 7):
+ *     POOL(L1 + l, K1 + c, dst_start + i, H1 + h, d) := block_r(l, c, i, h, d) */
+uint32_t ora_scatter_slice(const uint8_t *src, const ora_buf *B, uint8_t *dst,
+                           const ora_pool *Dp, const int64_t *sl,
+                           const int32_t *dst_pt, int64_t dst_pt_len,
+                           const int64_t *reqs, int64_t n_reqs)
+{
+    uint32_t err = 0;
+    if (sl[2] == 0 || sl[5] == 0 || sl[8] == 0)
+        return 0;
+    for (int64_t r = 0; r < n_reqs; ++r) {
+        const int64_t *q = reqs + 6 * r;
+        int64_t n = q[R_N];
+        if (!range_ok(q[R_DST_START], n) || q[R_SRC_START] != 0 ||
+            !block_ok(B, q[R_BUF], n)) {
+            err |= ORA_ERR_BAD_REQ;
+            continue;
+        }
+        for (int64_t i = 0; i < n; ++i) {
+            int64_t dp, ds;
+            int bad = resolve(Dp, dst_pt, dst_pt_len, q[R_DST_PT],
+                              q[R_DST_START] + i, ORA_ERR_DST_PAGE, &dp, &ds);
+            if (bad) {
+                err |= (uint32_t)bad;
+                continue;
+            }
+            for (int64_t l = 0; l < sl[2]; ++l)
+                for (int64_t c = 0; c < sl[5]; ++c)
+                    for (int64_t h = 0; h < sl[8]; ++h)
+                        for (int64_t d = 0; d < Dp->D; ++d)
+                            copy_elem(dst + Dp->e * pool_index(Dp, sl[1] + l, sl[4] + c,
+                                                               dp, ds, sl[7] + h, d),
+                                      src + B->e * buf_index(B, q[R_BUF], n, l, c, i, h, d),
+                                      Dp->e);
+        }
+    }
+    return err;
+}
+
 /* ------------------------------------------------------------------------
  * Chained page hashes (Sec. 5.1 "Chained Paged Hashing": each page's hash
  * encodes the hash of its predecessor, so two hashes are equal only when the

@@ -10,8 +10,10 @@ compiles it with gcc, loads it with ctypes and marshals numpy arrays.  What it
 computes is stated in the C file's header: Omni-Flow Sec. 4.1.1 (layer x page
 x slice addressing), Sec. 4.1.2 (conversion between the paged layout and the
 flat serialization), Sec. 4.1.4 (partial pages keep their other slots) and
-Sec. 5.2 (slot-to-page translation through a page table); and the chained
-page hashes of Sec. 5.1 (FNV-1a 64 page digests chained page by page).
+Sec. 5.2 (slot-to-page translation through a page table); slices of a pool
+(layer, kv and head ranges, Sec. 4.1.1 views) copied pool to pool or through
+a flat buffer; and the chained page hashes of Sec. 5.1 (FNV-1a 64 page
+digests chained page by page).
 
 Inputs are duck-typed: a pool shape is any object with integer attributes
 ``L C H D T N e`` and a ``layout`` name (``"LPCTHD"``, ``"LPCHTD"``,
@@ -119,6 +121,10 @@ class Oracle:
         lib.ora_scatter.restype = u32
         lib.ora_transfer_slice.argtypes = [vp, pp, vp, pp, vp, vp, i64, vp, i64, vp, i64]
         lib.ora_transfer_slice.restype = u32
+        lib.ora_gather_slice.argtypes = [vp, pp, vp, bp, vp, vp, i64, vp, i64]
+        lib.ora_gather_slice.restype = u32
+        lib.ora_scatter_slice.argtypes = [vp, bp, vp, pp, vp, vp, i64, vp, i64]
+        lib.ora_scatter_slice.restype = u32
         lib.ora_fnv1a64.argtypes = [vp, i64, ctypes.c_uint64]
         lib.ora_fnv1a64.restype = ctypes.c_uint64
         lib.ora_page_hashes.argtypes = [vp, i64, i64, i64, vp, i64, vp, i64]
@@ -165,6 +171,54 @@ class Oracle:
             _ptr(src), ctypes.byref(B), _ptr(dst), ctypes.byref(D),
             _ptr(dp), np.asarray(dst_pt).size, _ptr(rq), nr))
 
+
+    @staticmethod
+    def _buffer_slice(sl, pool_shape, buf_shape, pool_fields, buf_fields) -> np.ndarray:
+        """Check a slice against a pool and a buffer that holds exactly the
+        slice: the pool range inside the pool, the buffer offsets zero and
+        the buffer's L, C, H equal to the slice counts."""
+        sl = [int(x) for x in sl]
+        if len(sl) != 9:
+            raise ValueError("a slice has nine fields")
+        for k, (po, bo, cnt) in zip("LCH", (sl[0:3], sl[3:6], sl[6:9])):
+            p_off = po if pool_fields == 0 else bo
+            b_off = bo if pool_fields == 0 else po
+            if cnt < 0 or p_off < 0 or p_off + cnt > getattr(pool_shape, k):
+                raise ValueError(f"slice range {k} does not fit the pool")
+            if b_off != 0 or getattr(buf_shape, k) != cnt:
+                raise ValueError(f"the buffer must hold exactly the slice in {k}")
+        for k in ("D", "e"):
+            if getattr(pool_shape, k) != getattr(buf_shape, k):
+                raise ValueError(f"element shapes differ in {k}")
+        return np.asarray(sl, dtype=np.int64)
+
+    def gather_slice(self, src: np.ndarray, src_shape, dst: np.ndarray, buf_shape, sl,
+                     src_pt, reqs) -> int:
+        """Slice of a pool -> flat buffer holding exactly the slice (see
+        ora_gather_slice).  ``dst`` is updated in place."""
+        slc = self._buffer_slice(sl, src_shape, buf_shape, 0, 1)
+        _bytes(src, pool_elems(src_shape) * src_shape.e, "src")
+        _bytes(dst, buf_shape.cap * buf_shape.e, "dst", writable=True)
+        sp = _i32(src_pt)
+        rq, nr = _reqs(reqs)
+        S, B = _pool(src_shape), _buf(buf_shape)
+        return int(self.lib.ora_gather_slice(
+            _ptr(src), ctypes.byref(S), _ptr(dst), ctypes.byref(B), _ptr(slc),
+            _ptr(sp), np.asarray(src_pt).size, _ptr(rq), nr))
+
+    def scatter_slice(self, src: np.ndarray, buf_shape, dst: np.ndarray, dst_shape, sl,
+                      dst_pt, reqs) -> int:
+        """Flat buffer holding exactly the slice -> slice of a pool (see
+        ora_scatter_slice).  ``dst`` is updated in place."""
+        slc = self._buffer_slice(sl, dst_shape, buf_shape, 1, 0)
+        _bytes(src, buf_shape.cap * buf_shape.e, "src")
+        _bytes(dst, pool_elems(dst_shape) * dst_shape.e, "dst", writable=True)
+        dp = _i32(dst_pt)
+        rq, nr = _reqs(reqs)
+        B, D = _buf(buf_shape), _pool(dst_shape)
+        return int(self.lib.ora_scatter_slice(
+            _ptr(src), ctypes.byref(B), _ptr(dst), ctypes.byref(D), _ptr(slc),
+            _ptr(dp), np.asarray(dst_pt).size, _ptr(rq), nr))
 
     def transfer_slice(self, src: np.ndarray, src_shape, dst: np.ndarray, dst_shape, sl,
                        src_pt, dst_pt, reqs) -> int:

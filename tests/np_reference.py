@@ -84,3 +84,29 @@ def transfer_slice(src, S, dst, Dp, sl, src_pt, dst_pt, reqs) -> None:
         dp, ds = _where(np.asarray(dst_pt), do, d0, n, Dp.T)
         Vd[dl0:dl0 + nl, dp, dc0:dc0 + nc, ds, dh0:dh0 + nh, :] = \
             Vs[sl0:sl0 + nl, sp, sc0:sc0 + nc, ss, sh0:sh0 + nh, :]
+
+
+def gather_slice(src, S, dst, B, sl, src_pt, reqs) -> None:
+    """Slice of a pool -> buffer blocks [nl][nc][n][nh][D]: numpy slices of
+    the 6-D source view at the slice's source offsets."""
+    sl0, _dl0, nl, sc0, _dc0, nc, sh0, _dh0, nh = [int(x) for x in sl]
+    Vs = canon(src, S)
+    for so, _do, bo, s0, _d0, n in np.asarray(reqs, dtype=np.int64).reshape(-1, 6):
+        if n == 0:
+            continue
+        sp, ss = _where(np.asarray(src_pt), so, s0, n, S.T)
+        block(dst, B, bo, n)[...] = np.moveaxis(
+            Vs[sl0:sl0 + nl, sp, sc0:sc0 + nc, ss, sh0:sh0 + nh, :], 0, 2)
+
+
+def scatter_slice(src, B, dst, Dp, sl, dst_pt, reqs) -> None:
+    """Buffer blocks [nl][nc][n][nh][D] -> slice of a pool at the slice's
+    destination offsets."""
+    _sl0, dl0, nl, _sc0, dc0, nc, _sh0, dh0, nh = [int(x) for x in sl]
+    Vd = canon(dst, Dp)
+    for _so, do, bo, _s0, d0, n in np.asarray(reqs, dtype=np.int64).reshape(-1, 6):
+        if n == 0:
+            continue
+        dp, ds = _where(np.asarray(dst_pt), do, d0, n, Dp.T)
+        Vd[dl0:dl0 + nl, dp, dc0:dc0 + nc, ds, dh0:dh0 + nh, :] = \
+            np.moveaxis(block(src, B, bo, n), 2, 0)

@@ -608,6 +608,144 @@ def pin_slice_errors(O):
 
 
 # ---------------------------------------------------------------------------
+# slices through a flat buffer (gather_slice / scatter_slice)
+# ---------------------------------------------------------------------------
+
+def _slice_buffer_case(layout, sl, seed, T=4):
+    """A 3-layer, 2-kv, 4-head pool, three requests (shifted, ragged, empty)
+    and a buffer holding exactly the slice, blocks 16-byte aligned with gaps."""
+    rng = np.random.default_rng(seed)
+    P = PoolSpec(3, 2, 4, 8, T=T, N=12, e=2, layout=layout)
+    nl, nc, nh = sl[2], sl[5], sl[8]
+    reqs, pt, off, blocks = [], [], 0, []
+    perm = rng.permutation(P.N).astype(np.int32)
+    for s0, n in ((1, 7), (0, 5), (2, 0)):
+        k = -(-(s0 + n) // T)
+        reqs.append(_req(so=len(pt), bo=off, s0=s0, n=n))
+        pt.extend(perm[len(pt): len(pt) + k])
+        off += -(-(nl * nc * n * nh * 8) // 8) * 8 + 8
+    B = BufSpec(nl, nc, nh, 8, 2, cap=off)
+    return P, B, np.asarray(pt, np.int32), reqs
+
+
+BUFFER_SLICES = [(0, 0, 3, 0, 0, 2, 0, 0, 4),      # everything
+                 (0, 0, 3, 0, 0, 1, 0, 0, 4),      # K only
+                 (0, 0, 3, 1, 0, 1, 0, 0, 4),      # V only
+                 (1, 0, 2, 0, 0, 2, 2, 0, 2),      # layers 1-2, heads 2-3
+                 (2, 0, 1, 1, 0, 1, 3, 0, 1)]      # one row per token
+
+
+def pin_buffer_slice_numpy(O):
+    """gather_slice and scatter_slice against numpy slicing of the 6-D views,
+    for every layout and slice shape."""
+    for layout, k in itertools.product(LAYOUTS, range(len(BUFFER_SLICES))):
+        sl = BUFFER_SLICES[k]
+        P, B, pt, reqs = _slice_buffer_case(layout, sl, 50 + k)
+        pool = _pool_bytes(P, 60 + k)
+        got, want = np.zeros(B.nbytes, np.uint8), np.zeros(B.nbytes, np.uint8)
+        assert O.gather_slice(pool, P, got, B, sl, pt, reqs) == 0
+        npr.gather_slice(pool, P, want, B, sl, pt, reqs)
+        _same(got, want, f"gather_slice {layout} {sl}")
+        # scatter the buffer into a second pool at the slice's pool offsets
+        ssl = (0, sl[0], sl[2], 0, sl[3], sl[5], 0, sl[6], sl[8])
+        dpt = np.random.default_rng(70 + k).permutation(P.N).astype(np.int32)[: len(pt)]
+        srows = [_req(do=r[0], bo=r[2], d0=r[3], n=r[5]) for r in reqs]
+        d_got = prefill_bytes(P.nbytes, 5)
+        d_want = d_got.copy()
+        assert O.scatter_slice(got, B, d_got, P, ssl, dpt, srows) == 0
+        npr.scatter_slice(got, B, d_want, P, ssl, dpt, srows)
+        _same(d_got, d_want, f"scatter_slice {layout} {sl}")
+
+
+def pin_buffer_slice_full_and_parts(O):
+    """The full slice equals the plain gather; K-only and V-only blocks are
+    the two kv halves of the full block, and two head halves fill it."""
+    for layout in LAYOUTS:
+        full = BUFFER_SLICES[0]
+        P, B, pt, reqs = _slice_buffer_case(layout, full, 80)
+        pool = _pool_bytes(P, 81)
+        plain, whole = np.zeros(B.nbytes, np.uint8), np.zeros(B.nbytes, np.uint8)
+        assert O.gather(pool, P, plain, B, pt, reqs) == 0
+        assert O.gather_slice(pool, P, whole, B, full, pt, reqs) == 0
+        _same(whole, plain, f"full slice {layout}")
+        parts = {}
+        for name, sl in (("k", (0, 0, 3, 0, 0, 1, 0, 0, 4)), ("v", (0, 0, 3, 1, 0, 1, 0, 0, 4)),
+                         ("h0", (0, 0, 3, 0, 0, 2, 0, 0, 2)), ("h1", (0, 0, 3, 0, 0, 2, 2, 0, 2))):
+            Pp, Bp, ppt, preqs = _slice_buffer_case(layout, sl, 80)
+            buf = np.zeros(Bp.nbytes, np.uint8)
+            assert O.gather_slice(pool, P, buf, Bp, sl, ppt, preqs) == 0
+            parts[name] = (buf, Bp, preqs)
+        for (bo, n), r in zip([(q[2], q[5]) for q in reqs], range(len(reqs))):
+            if n == 0:
+                continue
+            W = npr.block(whole, B, bo, n)                       # [3][2][n][4][8]
+            K = npr.block(parts["k"][0], parts["k"][1], parts["k"][2][r][2], n)
+            V = npr.block(parts["v"][0], parts["v"][1], parts["v"][2][r][2], n)
+            H0 = npr.block(parts["h0"][0], parts["h0"][1], parts["h0"][2][r][2], n)
+            H1 = npr.block(parts["h1"][0], parts["h1"][1], parts["h1"][2][r][2], n)
+            assert np.array_equal(W[:, 0:1], K) and np.array_equal(W[:, 1:2], V), layout
+            assert np.array_equal(W[..., 0:2, :], H0) and np.array_equal(W[..., 2:4, :], H1), layout
+
+
+def pin_buffer_slice_roundtrip(O):
+    """V of layers 1-2 offloaded and restored into fresh pages: exactly that
+    part of the fresh pages changes, and it equals the source."""
+    for layout in LAYOUTS:
+        sl = (1, 0, 2, 1, 0, 1, 0, 0, 4)
+        P, B, pt, reqs = _slice_buffer_case(layout, sl, 90)
+        pool = _pool_bytes(P, 91)
+        buf = np.zeros(B.nbytes, np.uint8)
+        assert O.gather_slice(pool, P, buf, B, sl, pt, reqs) == 0
+        fresh = np.random.default_rng(92).permutation(P.N).astype(np.int32)[: len(pt)]
+        back = prefill_bytes(P.nbytes, 9)
+        before = back.copy()
+        srows = [_req(do=r[0], bo=r[2], d0=r[3], n=r[5]) for r in reqs]
+        assert O.scatter_slice(buf, B, back, P, (0, 1, 2, 0, 1, 1, 0, 0, 4), fresh, srows) == 0
+        Vs, Vb, V0 = npr.canon(pool, P), npr.canon(back, P), npr.canon(before, P)
+        changed = np.zeros(Vb.shape[:5], bool)
+        for (so, do, bo, s0, d0, n), in zip([(r[0], r[1], r[2], r[3], r[4], r[5]) for r in reqs]):
+            for i in range(n):
+                q = s0 + i
+                sp, ss = pt[so + q // P.T], q % P.T
+                dp, ds = fresh[so + q // P.T], q % P.T
+                assert np.array_equal(Vb[1:3, dp, 1, ds], Vs[1:3, sp, 1, ss]), layout
+                changed[1:3, dp, 1, ds] = True
+        assert np.array_equal(Vb[~changed], V0[~changed]), layout
+
+
+def pin_buffer_slice_errors(O):
+    """The plain gather/scatter error rules hold for slices, and a slice with
+    a zero count copies and checks nothing."""
+    sl = (0, 0, 1, 1, 0, 1, 0, 0, 2)
+    P = PoolSpec(2, 2, 2, 8, T=4, N=4, e=2, layout="LPCTHD")
+    B = BufSpec(1, 1, 2, 8, 2, cap=1 * 1 * 8 * 2 * 8)
+    pool = _pool_bytes(P, 3)
+    for pt, row, bits in (([0, 4], _req(n=8), ERR_SRC_PAGE), ([0], _req(n=8), ERR_PT_RANGE),
+                          ([0, 1], _req(n=8, d0=1), ERR_BAD_REQ),
+                          ([0, 1], _req(n=8, bo=4), ERR_BAD_REQ),
+                          ([0, 1], _req(n=9), ERR_BAD_REQ),
+                          ([0, 1], _req(n=8), 0)):
+        buf = np.full(B.nbytes, 0xEE, np.uint8)
+        assert O.gather_slice(pool, P, buf, B, sl, pt, [row]) == bits, (pt, row)
+        if bits == ERR_BAD_REQ:
+            assert (buf == 0xEE).all()
+    buf = np.full(B.nbytes, 0xEE, np.uint8)
+    d = prefill_bytes(P.nbytes, 4)
+    before = d.copy()
+    for rule in ((0, 0, 1, 0, 1, 1, 0, 0, 2),):
+        assert O.scatter_slice(buf, B, d, P, rule, [-1, 4], [_req(n=8)]) == ERR_DST_PAGE
+        assert O.scatter_slice(buf, B, d, P, rule, [-1], [_req(n=8)]) == ERR_DST_PAGE | ERR_PT_RANGE
+        assert O.scatter_slice(buf, B, d, P, rule, [0, 1], [_req(n=8, s0=1)]) == ERR_BAD_REQ
+    _same(d, before, "skipped positions written")
+    for empty in ((0, 0, 0, 1, 0, 1, 0, 0, 2), (0, 0, 1, 1, 0, 0, 0, 0, 2), (0, 0, 1, 1, 0, 1, 0, 0, 0)):
+        Be = BufSpec(empty[2], empty[5], empty[8], 8, 2, cap=64)
+        assert O.gather_slice(pool, P, np.zeros(Be.nbytes, np.uint8), Be, empty, [9], [_req(n=-3)]) == 0
+        se = (0, empty[0], empty[2], 0, empty[3], empty[5], 0, empty[6], empty[8])
+        assert O.scatter_slice(np.zeros(Be.nbytes, np.uint8), Be, d, P, se, [-1], [_req(n=8)]) == 0
+    _same(d, before, "an empty slice wrote")
+
+
+# ---------------------------------------------------------------------------
 # copy-on-write inside one pool
 # ---------------------------------------------------------------------------
 
@@ -732,7 +870,9 @@ PINS = [pin_hand_example, pin_hand_example_plchtd, pin_numpy_transfer,
         pin_numpy_transfer_widths, pin_numpy_gather_scatter, pin_identity_tables,
         pin_roundtrip, pin_bijection, pin_errors, pin_max_position, pin_tiny_workload,
         pin_slice_hand_example, pin_slice_numpy, pin_slice_decomposes_transfer,
-        pin_slice_tp_roundtrip, pin_slice_errors, pin_same_pool_copy_on_write,
+        pin_slice_tp_roundtrip, pin_slice_errors, pin_buffer_slice_numpy,
+        pin_buffer_slice_full_and_parts, pin_buffer_slice_roundtrip, pin_buffer_slice_errors,
+        pin_same_pool_copy_on_write,
         pin_fnv_published_vectors, pin_hash_definition, pin_hash_prefix_property,
         pin_hash_continuation, pin_hash_partial_last_page, pin_hash_errors]
 

@@ -32,6 +32,11 @@ T_XFER_H = ("for (int64_t h = 0; h < S->H; ++h)\n"
             "                        for (int64_t d = 0; d < S->D; ++d)\n"
             "                            copy_elem(dst + Dp->e * pool_index(Dp")
 
+T_GS_POOL = ("src + S->e * pool_index(S, sl[0] + l, sl[3] + c,\n"
+             "                                                              sp, ss, sl[6] + h, d)")
+T_SS_POOL = ("copy_elem(dst + Dp->e * pool_index(Dp, sl[1] + l, sl[4] + c,\n"
+             "                                                               dp, ds, sl[7] + h, d)")
+
 MUTANTS = {
     "lpcthd_slot_head_swapped": (T_LPCTHD, T_LPCTHD.replace(
         "* P->T + s) * P->H + h)", "* P->H + h) * P->T + s)")),
@@ -81,8 +86,20 @@ MUTANTS = {
     "slice_dst_head_from_src_offset": ("sl[7] + h", "sl[6] + h"),
     "slice_src_kv_offset_dropped": ("sl[3] + c", "c"),
     "slice_one_layer_short": ("l < sl[2]", "l + 1 < sl[2]"),
-    "slice_heads_of_the_pool": ("h < sl[8]", "h < S->H"),
+    "slice_heads_of_the_pool": (
+        "h < sl[8]; ++h)\n                        for (int64_t d = 0; d < S->D; ++d)",
+        "h < S->H; ++h)\n                        for (int64_t d = 0; d < S->D; ++d)"),
+    "scatter_slice_heads_of_the_pool": (
+        "h < sl[8]; ++h)\n                        for (int64_t d = 0; d < Dp->D; ++d)",
+        "h < Dp->H; ++h)\n                        for (int64_t d = 0; d < Dp->D; ++d)"),
     "empty_slice_checked": ("    if (sl[2] == 0 || sl[5] == 0 || sl[8] == 0)\n        return 0;\n", ""),
+    "gather_slice_layer_from_buffer_offset": (
+        T_GS_POOL, T_GS_POOL.replace("sl[0] + l", "sl[1] + l")),
+    "gather_slice_head_offset_dropped": (T_GS_POOL, T_GS_POOL.replace("sl[6] + h", "h")),
+    "scatter_slice_kv_from_buffer_offset": (
+        T_SS_POOL, T_SS_POOL.replace("sl[4] + c", "sl[3] + c")),
+    "scatter_slice_one_layer_short": (
+        T_SS_POOL, T_SS_POOL.replace("sl[1] + l", "sl[1] + l + (l > 0)")),
     "fnv1_instead_of_fnv1a": ("        h ^= p[i];\n        h *= FNV_PRIME;",
                               "        h *= FNV_PRIME;\n        h ^= p[i];"),
     "chain_pair_swapped": ("le64(pair, h);\n            le64(pair + 8, c);",
@@ -93,11 +110,16 @@ MUTANTS = {
     "hash_out_shifted": ("out[out_off + j] = h;", "out[out_off + pages - 1 - j] = h;"),
     "hash_bounds_unchecked": ("off + n > payload_positions ||", "0 ||"),
 }
-# Sites that occur in both the pool -> pool and the slice copy: mutate one
-# occurrence at a time (0: ora_transfer, 1: ora_transfer_slice).
-SHARED = ("source_position_from_dst_start", "dst_position_from_src_start",
-          "source_resolved_first")
-CASES = sorted([(name, 0) for name in MUTANTS] + [(name, 1) for name in SHARED])
+# Sites that occur in more than one function: each occurrence is mutated on
+# its own, in source order (ora_transfer, ora_gather, ora_scatter,
+# ora_transfer_slice, ora_gather_slice, ora_scatter_slice).
+OCCURRENCES = {"source_position_from_dst_start": 2, "dst_position_from_src_start": 2,
+               "source_resolved_first": 2, "scatter_tokens_reversed": 2,
+               "gather_ignores_dst_start": 2, "slice_dst_layer_from_src_offset": 2,
+               "slice_dst_head_from_src_offset": 2, "slice_src_kv_offset_dropped": 2,
+               "slice_one_layer_short": 3, "slice_heads_of_the_pool": 2,
+               "empty_slice_checked": 3}
+CASES = sorted((name, k) for name in MUTANTS for k in range(OCCURRENCES.get(name, 1)))
 
 
 def _run_pins(lib):
@@ -115,7 +137,7 @@ def test_real_oracle_passes_pins_in_child():
 def test_mutant_is_caught(name, occurrence, tmp_path):
     old, new = MUTANTS[name]
     text = open(kvx_oracle.SOURCE).read()
-    want = 2 if name in SHARED else 1
+    want = OCCURRENCES.get(name, 1)
     assert text.count(old) == want, f"mutation site for {name} must occur {want} time(s)"
     assert old != new
     at = -1
