@@ -78,7 +78,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="handoff",
                     choices=["handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
-                             "handoff_layered", "small_requests", "page_hash"])
+                             "handoff_layered", "small_requests", "host_tier_v", "page_hash"])
     ap.add_argument("--cpu-layers", type=int, default=16,
                     help="layers of the workload the CPU oracle runs (0: skip)")
     ap.add_argument("--cpu-threads", type=int, default=16,
@@ -163,8 +163,12 @@ def main() -> int:
                                    d["reqs"], errw)
         elif st.op == "transfer":
             kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"], errw)
+        elif st.op == "gather" and st.slice is not None:
+            kvx.kvx_gather_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["spt"], d["reqs"], errw)
         elif st.op == "gather":
             kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, d["spt"], d["reqs"], errw)
+        elif st.slice is not None:
+            kvx.kvx_scatter_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["dpt"], d["reqs"], errw)
         else:
             kvx.kvx_scatter(mem[st.src], S, mem[st.dst], D, d["dpt"], d["reqs"], errw)
 

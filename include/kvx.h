@@ -217,6 +217,36 @@ int kvx_scatter(const kvx_buf *src, const kvx_pool *dst,
                 const kvx_req *reqs, int32_t n_reqs,
                 uint32_t *dev_err, void *stream);
 
+/* Slice of a pool -> flat buffer that holds exactly the slice (Sec. 4.1.2
+ * migration of a Sec. 4.1.1 view: offload only V, a layer range, or one
+ * tensor-parallel head range).  For every record r, token i < n_tokens,
+ * l < num_layers, c < num_kv, h < num_heads and every d:
+ *   block_r(l, c, i, h, d)
+ *     := src(src_layer0 + l, src_kv0 + c, src_start + i, src_head0 + h, d)
+ * where block_r is the record's block [num_layers][num_kv][n_tokens]
+ * [num_heads][head_dim] at buf_off.
+ * - The buffer's num_layers, num_kv and num_heads must equal the slice's
+ *   counts (KVX_ERR_SHAPE otherwise), its head_dim and elem_bytes the
+ *   pool's; the slice's destination offsets must be 0 and its source range
+ *   must lie inside the pool (KVX_ERR_RANGE otherwise).
+ * - Every other rule, argument and device error bit is kvx_gather's, which
+ *   is this call with the full slice. */
+int kvx_gather_slice(const kvx_pool *src, const kvx_buf *dst, const kvx_slice *slice,
+                     const int32_t *src_pt, int64_t src_pt_len,
+                     const kvx_req *reqs, int32_t n_reqs,
+                     uint32_t *dev_err, void *stream);
+
+/* Flat buffer that holds exactly a slice -> that slice of a pool (the onload
+ * of kvx_gather_slice):
+ *   dst(dst_layer0 + l, dst_kv0 + c, dst_start + i, dst_head0 + h, d)
+ *     := block_r(l, c, i, h, d)
+ * The slice's source offsets must be 0 and its destination range must lie
+ * inside the pool; otherwise as kvx_gather_slice and kvx_scatter. */
+int kvx_scatter_slice(const kvx_buf *src, const kvx_pool *dst, const kvx_slice *slice,
+                      const int32_t *dst_pt, int64_t dst_pt_len,
+                      const kvx_req *reqs, int32_t n_reqs,
+                      uint32_t *dev_err, void *stream);
+
 /* One chained-hash request (32 bytes). */
 typedef struct kvx_hash_req {
     int64_t payload_off;  /* first position of the request in the payload */

@@ -145,3 +145,28 @@ def gather_scatter_layer(pool_before: np.ndarray, S, buf_t, B, pool_after: np.nd
     ok_s = O.scatter(want_buf, b1, want_pool, s1, scatter.dst_pt, s_rows) == 0 and \
         np.array_equal(pool_after, want_pool)
     return ok_g, ok_s
+
+
+def gather_scatter_slice_layer(pool_before: np.ndarray, S, buf_t, B, pool_after: np.ndarray,
+                               gather, scatter, l: int) -> tuple[bool, bool]:
+    """Layer l of a sliced gather and scatter through a buffer that holds
+    exactly the slice (l counts from the slice's first layer; the gather
+    reads pool layer gather.slice[0] + l and the scatter writes pool layer
+    scatter.slice[1] + l, which ``pool_before`` / ``pool_after`` hold)."""
+    gs, ss = list(gather.slice), list(scatter.slice)
+    s1 = one_layer(S)
+    blocks = [(int(r[2]), int(r[5])) for r in gather.reqs]
+    got_buf, offs = buf_layer(buf_t, B, l, blocks)
+    b1 = dataclasses.replace(B, L=1, cap=got_buf.nbytes // B.e)
+    g_rows = gather.reqs.copy()
+    g_rows[:, 2] = offs
+    want_buf = np.zeros_like(got_buf)
+    O = kvx_oracle.default()
+    ok_g = O.gather_slice(pool_before, s1, want_buf, b1, [0, 0, 1] + gs[3:], gather.src_pt,
+                          g_rows) == 0 and np.array_equal(got_buf, want_buf)
+    s_rows = scatter.reqs.copy()
+    s_rows[:, 2] = offs
+    want_pool = pool_before.copy()
+    ok_s = O.scatter_slice(want_buf, b1, want_pool, s1, [0, 0, 1] + ss[3:], scatter.dst_pt,
+                           s_rows) == 0 and np.array_equal(pool_after, want_pool)
+    return ok_g, ok_s

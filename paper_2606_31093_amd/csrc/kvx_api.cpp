@@ -350,6 +350,87 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
     return KVX_OK;
 }
 
+// A buffer that holds exactly a slice of a pool: the pool's range inside the
+// pool, the buffer-side offsets zero and the buffer's layer, kv and head
+// counts equal to the slice's.  `pool_is_src` picks which offsets are the
+// pool's (source fields for a gather, destination fields for a scatter).
+int check_buffer_slice(const kvx_slice &sl, const Shape &pool, const Shape &buf, bool pool_is_src) {
+    if (pool.D != buf.D || pool.e != buf.e)
+        return fail(KVX_ERR_SHAPE, "head_dim/elem_bytes differ: (%d, %d) vs (%d, %d)", pool.D, pool.e,
+                    buf.D, buf.e);
+    if (sl.reserved != 0) return fail(KVX_ERR_RANGE, "slice: reserved field must be 0");
+    const struct {
+        const char *what;
+        int32_t p0, b0, n, pmax, bn;
+    } r[3] = {{"layer", pool_is_src ? sl.src_layer0 : sl.dst_layer0,
+               pool_is_src ? sl.dst_layer0 : sl.src_layer0, sl.num_layers, pool.L, buf.L},
+              {"kv", pool_is_src ? sl.src_kv0 : sl.dst_kv0, pool_is_src ? sl.dst_kv0 : sl.src_kv0,
+               sl.num_kv, pool.C, buf.C},
+              {"head", pool_is_src ? sl.src_head0 : sl.dst_head0,
+               pool_is_src ? sl.dst_head0 : sl.src_head0, sl.num_heads, pool.H, buf.H}};
+    for (const auto &x : r) {
+        if (x.n < 0 || x.p0 < 0 || (int64_t)x.p0 + x.n > x.pmax)
+            return fail(KVX_ERR_RANGE, "slice %s range [%d, %lld) outside the pool's %d", x.what, x.p0,
+                        (long long)x.p0 + x.n, x.pmax);
+        if (x.b0 != 0)
+            return fail(KVX_ERR_RANGE, "slice %s offset on the buffer side must be 0 (got %d)", x.what,
+                        x.b0);
+        if (x.n != x.bn)
+            return fail(KVX_ERR_SHAPE, "the buffer holds %d %s(s), the slice %d", x.bn, x.what, x.n);
+    }
+    return KVX_OK;
+}
+
+// Pool <-> flat buffer.  `op` is OP_GATHER (pool -> buffer) or OP_SCATTER
+// (buffer -> pool); slice == NULL moves everything between equal shapes.
+int buffer_impl(int op, const kvx_pool *pool, const kvx_buf *buf, const kvx_slice *slice,
+                const int32_t *pt, int64_t pt_len, const kvx_req *reqs, int32_t n_reqs,
+                uint32_t *dev_err, void *stream) {
+    const bool gather = op == kvx::OP_GATHER;
+    const char *pname = gather ? "src" : "dst", *bname = gather ? "dst" : "src";
+    const char *tname = gather ? "src_pt" : "dst_pt";
+    Shape ps, bs;
+    int st;
+    if (gather) {
+        if ((st = check_pool(pool, pname, ps))) return st;
+        if ((st = check_buf(buf, bname, bs))) return st;
+    } else {
+        if ((st = check_buf(buf, bname, bs))) return st;
+        if ((st = check_pool(pool, pname, ps))) return st;
+    }
+    kvx_slice sl;
+    if (slice) {
+        sl = *slice;
+        if ((st = check_buffer_slice(sl, ps, bs, gather))) return st;
+    } else {
+        if ((st = same_shape(ps, bs))) return st;
+        sl = kvx_slice{0, 0, ps.L, 0, 0, ps.C, 0, 0, ps.H, 0};
+    }
+    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
+    if ((st = check_table(pt, pt_len, tname))) return st;
+    if (n_reqs == 0) return KVX_OK;
+    Views v;
+    if (gather)
+        st = view_all(pool->base, buf->base, pt, pt_len, nullptr, 0, reqs, dev_err, v);
+    else
+        st = view_all(buf->base, pool->base, nullptr, 0, pt, pt_len, reqs, dev_err, v);
+    if (st) return st;
+    const int32_t l0 = gather ? sl.src_layer0 : sl.dst_layer0;
+    const int32_t c0 = gather ? sl.src_kv0 : sl.dst_kv0;
+    const int32_t h0 = gather ? sl.src_head0 : sl.dst_head0;
+    kvx::Params P{};
+    P.op = op;
+    if (gather) {
+        P.src = pool_side(pool, v.src, v.src_pt, pt_len, l0, c0, h0, sl.num_heads);
+        P.dst = buf_side(buf, v.dst);
+    } else {
+        P.src = buf_side(buf, v.src);
+        P.dst = pool_side(pool, v.dst, v.dst_pt, pt_len, l0, c0, h0, sl.num_heads);
+    }
+    finish_params(P, Shape{sl.num_layers, sl.num_kv, sl.num_heads, ps.D, ps.e}, v, n_reqs);
+    return enqueue(P, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -375,45 +456,33 @@ int kvx_transfer_slice(const kvx_pool *src, const kvx_pool *dst, const kvx_slice
 int kvx_gather(const kvx_pool *src, const kvx_buf *dst, const int32_t *src_pt, int64_t src_pt_len,
                const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err, void *stream) {
     g_last_error.clear();
-    Shape ss, ds;
-    int st;
-    if ((st = check_pool(src, "src", ss))) return st;
-    if ((st = check_buf(dst, "dst", ds))) return st;
-    if ((st = same_shape(ss, ds))) return st;
-    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
-    if ((st = check_table(src_pt, src_pt_len, "src_pt"))) return st;
-    if (n_reqs == 0) return KVX_OK;
-    Views v;
-    if ((st = view_all(src->base, dst->base, src_pt, src_pt_len, nullptr, 0, reqs, dev_err, v)))
-        return st;
-    kvx::Params P{};
-    P.op = kvx::OP_GATHER;
-    P.src = pool_side(src, v.src, v.src_pt, src_pt_len, 0, 0, 0, ss.H);
-    P.dst = buf_side(dst, v.dst);
-    finish_params(P, ss, v, n_reqs);
-    return enqueue(P, stream);
+    return buffer_impl(kvx::OP_GATHER, src, dst, nullptr, src_pt, src_pt_len, reqs, n_reqs, dev_err,
+                       stream);
 }
 
 int kvx_scatter(const kvx_buf *src, const kvx_pool *dst, const int32_t *dst_pt, int64_t dst_pt_len,
                 const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err, void *stream) {
     g_last_error.clear();
-    Shape ss, ds;
-    int st;
-    if ((st = check_buf(src, "src", ss))) return st;
-    if ((st = check_pool(dst, "dst", ds))) return st;
-    if ((st = same_shape(ss, ds))) return st;
-    if ((st = check_common(reqs, n_reqs, dev_err))) return st;
-    if ((st = check_table(dst_pt, dst_pt_len, "dst_pt"))) return st;
-    if (n_reqs == 0) return KVX_OK;
-    Views v;
-    if ((st = view_all(src->base, dst->base, nullptr, 0, dst_pt, dst_pt_len, reqs, dev_err, v)))
-        return st;
-    kvx::Params P{};
-    P.op = kvx::OP_SCATTER;
-    P.src = buf_side(src, v.src);
-    P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, 0, 0, 0, ds.H);
-    finish_params(P, ss, v, n_reqs);
-    return enqueue(P, stream);
+    return buffer_impl(kvx::OP_SCATTER, dst, src, nullptr, dst_pt, dst_pt_len, reqs, n_reqs, dev_err,
+                       stream);
+}
+
+int kvx_gather_slice(const kvx_pool *src, const kvx_buf *dst, const kvx_slice *slice,
+                     const int32_t *src_pt, int64_t src_pt_len, const kvx_req *reqs, int32_t n_reqs,
+                     uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    if (!slice) return fail(KVX_ERR_NULL, "slice is NULL");
+    return buffer_impl(kvx::OP_GATHER, src, dst, slice, src_pt, src_pt_len, reqs, n_reqs, dev_err,
+                       stream);
+}
+
+int kvx_scatter_slice(const kvx_buf *src, const kvx_pool *dst, const kvx_slice *slice,
+                      const int32_t *dst_pt, int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs,
+                      uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    if (!slice) return fail(KVX_ERR_NULL, "slice is NULL");
+    return buffer_impl(kvx::OP_SCATTER, dst, src, slice, dst_pt, dst_pt_len, reqs, n_reqs, dev_err,
+                       stream);
 }
 
 int kvx_transfer_layered(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,

@@ -4,8 +4,8 @@ Every step of the copy runs in the library's HIP kernels.  PyTorch supplies
 device memory and the stream: tensors are passed as raw pointers and the
 kernels run on ``torch.cuda.current_stream()`` unless a stream is given.
 The functions keep the C names: ``kvx_transfer``, ``kvx_transfer_slice``,
-``kvx_transfer_layered``, ``kvx_gather``, ``kvx_scatter`` and
-``kvx_page_hashes``.  A missing or unloadable library raises; there is no
+``kvx_transfer_layered``, ``kvx_gather``, ``kvx_scatter``,
+``kvx_gather_slice``, ``kvx_scatter_slice`` and ``kvx_page_hashes``.  A missing or unloadable library raises; there is no
 fallback path.
 
 Pool and buffer shapes are duck-typed: a pool shape has integer attributes
@@ -105,8 +105,11 @@ def lib() -> ctypes.CDLL:
                                            i32, i32, ctypes.POINTER(vp), i32, vp, vp]
         L.kvx_gather.argtypes = [pp, bp, vp, i64, vp, i32, vp, vp]
         L.kvx_scatter.argtypes = [bp, pp, vp, i64, vp, i32, vp, vp]
+        sp = ctypes.POINTER(Slice)
+        L.kvx_gather_slice.argtypes = [pp, bp, sp, vp, i64, vp, i32, vp, vp]
+        L.kvx_scatter_slice.argtypes = [bp, pp, sp, vp, i64, vp, i32, vp, vp]
         for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_transfer_layered, L.kvx_gather,
-                  L.kvx_scatter):
+                  L.kvx_scatter, L.kvx_gather_slice, L.kvx_scatter_slice):
             f.restype = ctypes.c_int
         L.kvx_page_hashes.argtypes = [vp, i64, i32, i32, vp, i32, vp, i64, vp, vp]
         L.kvx_page_hashes.restype = ctypes.c_int
@@ -310,6 +313,33 @@ def kvx_scatter(src, buf_spec, dst, dst_spec, dst_pt, reqs, dev_err=None, stream
     _table(dst_pt, "dst_pt"), _err_word(dev_err)
     _check(lib().kvx_scatter(ctypes.byref(B), ctypes.byref(D), _ptr(dst_pt), _len(dst_pt),
                              _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
+
+
+def kvx_gather_slice(src, src_spec, dst, buf_spec, sl, src_pt, reqs, dev_err=None,
+                     stream=None) -> None:
+    """Slice of a pool -> flat buffer holding exactly the slice (see
+    kvx_gather_slice in include/kvx.h).  ``sl`` is a ``Slice`` or the nine
+    range fields."""
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, buf_spec.cap * buf_spec.e, "dst")
+    S, B, X = pool_desc(src_spec, src), buf_desc(buf_spec, dst), slice_desc(sl)
+    _table(src_pt, "src_pt"), _err_word(dev_err)
+    _check(lib().kvx_gather_slice(ctypes.byref(S), ctypes.byref(B), ctypes.byref(X), _ptr(src_pt),
+                                  _len(src_pt), _ptr(reqs), _n_reqs(reqs), _ptr(dev_err),
+                                  _stream(stream)))
+
+
+def kvx_scatter_slice(src, buf_spec, dst, dst_spec, sl, dst_pt, reqs, dev_err=None,
+                      stream=None) -> None:
+    """Flat buffer holding exactly a slice -> that slice of a pool (see
+    kvx_scatter_slice in include/kvx.h)."""
+    _need(src, buf_spec.cap * buf_spec.e, "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    B, D, X = buf_desc(buf_spec, src), pool_desc(dst_spec, dst), slice_desc(sl)
+    _table(dst_pt, "dst_pt"), _err_word(dev_err)
+    _check(lib().kvx_scatter_slice(ctypes.byref(B), ctypes.byref(D), ctypes.byref(X), _ptr(dst_pt),
+                                   _len(dst_pt), _ptr(reqs), _n_reqs(reqs), _ptr(dev_err),
+                                   _stream(stream)))
 
 
 def pack_hash_reqs(rows) -> np.ndarray:

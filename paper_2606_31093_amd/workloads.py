@@ -259,6 +259,29 @@ def host_tier(small: bool = False) -> Workload:
                     value_seed=2005, prefill_tag=5, host_sides=("buf",))
 
 
+def host_tier_v(small: bool = False) -> Workload:
+    """The host-tier offload/onload of the same pages, V only (Sec. 4.1.3:
+    K and V of a page may live on different nodes or tiers): the V half of
+    each page is gathered into a pinned buffer that holds only V, then
+    scattered into the V half of fresh pages."""
+    wl = host_tier(small)
+    g, s = wl.steps
+    P, B = wl.sides["A"], wl.sides["buf"]
+    n = int(g.reqs[0][5])
+    block = P.L * 1 * n * P.H * P.D
+    nreq = len(g.reqs)
+    buf = BufSpec(P.L, 1, P.H, P.D, P.e, cap=nreq * block)
+    g_rows = [[r[0], 0, i * block, 0, 0, n] for i, r in enumerate(g.reqs)]
+    s_rows = [[0, r[1], i * block, 0, 0, n] for i, r in enumerate(s.reqs)]
+    steps = [Step("gather", "A", "buf", g.src_pt, None, _reqs(g_rows),
+                  slice=(0, 0, P.L, 1, 0, 1, 0, 0, P.H)),
+             Step("scatter", "buf", "A", None, s.dst_pt, _reqs(s_rows),
+                  slice=(0, 0, P.L, 0, 1, 1, 0, 0, P.H))]
+    return Workload("host_tier_v", wl.title.replace("offload/onload", "V-only offload/onload"),
+                    {"A": P, "buf": buf}, steps, value_seed=2015, prefill_tag=15,
+                    host_sides=("buf",))
+
+
 def tp_reshard(small: bool = False) -> Workload:
     """Tensor-parallel reshard of the handoff cache: a consumer running with
     two tensor-parallel ranks holds 4 of the 8 KV heads per pool; this moves
@@ -348,7 +371,7 @@ def small_requests(small: bool = False) -> Workload:
 
 
 NAMES = ("tiny", "handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
-         "handoff_layered", "small_requests")
+         "handoff_layered", "small_requests", "host_tier_v")
 
 
 def get(name: str, small: bool = False) -> Workload:
@@ -358,7 +381,7 @@ def get(name: str, small: bool = False) -> Workload:
     return {"handoff": handoff, "relayout": relayout, "mla": mla,
             "host_tier": host_tier, "tp_reshard": tp_reshard,
             "cow_fork": cow_fork, "handoff_layered": handoff_layered,
-            "small_requests": small_requests}[name](small=small)
+            "small_requests": small_requests, "host_tier_v": host_tier_v}[name](small=small)
 
 
 def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:

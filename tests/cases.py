@@ -237,3 +237,49 @@ def random_gs_case(seed: int) -> Workload:
 
 
 RANDOM_GS_CASES = 100
+
+
+def buffer_slice_case(ls, ld, T, src_lch, dst_lch, gsl, dst_off, seed, *, pinned=False,
+                      D=64, e=2) -> Workload:
+    """A slice of pool A gathered into a buffer that holds exactly the slice,
+    then scattered into a slice of pool B (another shape and layout) at
+    ``dst_off`` = (layer0, kv0, head0).  ``gsl`` is the gather's nine-field
+    slice (its buffer-side offsets 0)."""
+    rng = np.random.default_rng(seed)
+    (Ls, Cs, Hs), (Ld, Cd, Hd) = src_lch, dst_lch
+    nl, nc, nh = gsl[2], gsl[5], gsl[8]
+    align = 16 // e
+    ns, starts, dstarts = [3 * T + 2, 1, 0, 2 * T], [T // 2 + 1, T - 1, 0, 0], [1, 0, 3, T]
+    blocks, off = [], align
+    for n in ns:
+        blocks.append(off)
+        off += _cdiv(nl * nc * n * nh * D, align) * align + align
+    B = BufSpec(nl, nc, nh, D, e, cap=off)
+    S = PoolSpec(Ls, Cs, Hs, D, T=T, N=sum(_cdiv(s + n, T) for n, s in zip(ns, starts)) + 2, e=e,
+                 layout=ls)
+    Dp = PoolSpec(Ld, Cd, Hd, D, T=T, N=sum(_cdiv(s + n, T) for n, s in zip(ns, dstarts)) + 2,
+                  e=e, layout=ld)
+    perm, dperm = rng.permutation(S.N).astype(np.int32), rng.permutation(Dp.N).astype(np.int32)
+    g_rows, s_rows, pt, dpt = [], [], [], []
+    for n, s0, d0, bo in zip(ns, starts, dstarts, blocks):
+        g_rows.append([len(pt), 0, bo, s0, 0, n])
+        s_rows.append([0, len(dpt), bo, 0, d0, n])
+        pt.extend(perm[len(pt): len(pt) + _cdiv(s0 + n, T)])
+        dpt.extend(dperm[len(dpt): len(dpt) + _cdiv(d0 + n, T)])
+    ssl = (0, dst_off[0], nl, 0, dst_off[1], nc, 0, dst_off[2], nh)
+    steps = [Step("gather", "A", "buf", np.asarray(pt, np.int32), None,
+                  np.asarray(g_rows, np.int64), slice=tuple(gsl)),
+             Step("scatter", "buf", "B", None, np.asarray(dpt, np.int32),
+                  np.asarray(s_rows, np.int64), slice=ssl)]
+    return Workload("case", f"buffer slice {gsl} {ls} {src_lch} -> {ld} {dst_lch} at {dst_off}",
+                    {"A": S, "buf": B, "B": Dp}, steps, value_seed=seed, prefill_tag=seed & 0xFF,
+                    host_sides=("buf",) if pinned else ())
+
+
+# (source L, C, H), (destination L, C, H), gather slice, destination offsets
+BUFFER_SLICES = [((3, 2, 4), (3, 2, 4), (0, 0, 3, 0, 0, 2, 0, 0, 4), (0, 0, 0)),   # whole pool
+                 ((3, 2, 4), (3, 1, 4), (0, 0, 3, 1, 0, 1, 0, 0, 4), (0, 0, 0)),   # V only
+                 ((3, 2, 4), (3, 2, 4), (0, 0, 3, 0, 0, 1, 0, 0, 4), (0, 1, 0)),   # K into V
+                 ((4, 2, 8), (2, 2, 4), (2, 0, 2, 0, 0, 2, 4, 0, 4), (0, 0, 0)),   # TP shard of a stage
+                 ((2, 1, 3), (3, 1, 5), (0, 0, 2, 0, 0, 1, 1, 0, 2), (1, 0, 3)),   # into a larger pool
+                 ((2, 2, 2), (2, 2, 2), (1, 0, 1, 1, 0, 1, 1, 0, 1), (0, 0, 0))]   # one row per token

@@ -35,8 +35,12 @@ def run_oracle(wl, init: dict, reqs_override=None) -> tuple[dict, list]:
             e = O.transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, st.src_pt, st.dst_pt, reqs)
         elif st.op == "transfer":
             e = O.transfer(mem[st.src], S, mem[st.dst], D, st.src_pt, st.dst_pt, reqs)
+        elif st.op == "gather" and st.slice is not None:
+            e = O.gather_slice(mem[st.src], S, mem[st.dst], D, st.slice, st.src_pt, reqs)
         elif st.op == "gather":
             e = O.gather(mem[st.src], S, mem[st.dst], D, st.src_pt, reqs)
+        elif st.slice is not None:
+            e = O.scatter_slice(mem[st.src], S, mem[st.dst], D, st.slice, st.dst_pt, reqs)
         else:
             e = O.scatter(mem[st.src], S, mem[st.dst], D, st.dst_pt, reqs)
         errs.append(e)
@@ -79,8 +83,12 @@ def run_gpu(wl, init: dict, raw_reqs=None) -> tuple[dict, list]:
             kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, spt, dpt, reqs, err)
         elif st.op == "transfer":
             kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs, err)
+        elif st.op == "gather" and st.slice is not None:
+            kvx.kvx_gather_slice(mem[st.src], S, mem[st.dst], D, st.slice, spt, reqs, err)
         elif st.op == "gather":
             kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, spt, reqs, err)
+        elif st.slice is not None:
+            kvx.kvx_scatter_slice(mem[st.src], S, mem[st.dst], D, st.slice, dpt, reqs, err)
         else:
             kvx.kvx_scatter(mem[st.src], S, mem[st.dst], D, dpt, reqs, err)
         torch.cuda.synchronize()

@@ -10,7 +10,7 @@ import bench
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 WORKLOADS = ["handoff", "relayout", "mla", "host_tier", "tp_reshard", "cow_fork",
-             "handoff_layered", "page_hash"]
+             "handoff_layered", "small_requests", "host_tier_v", "page_hash"]
 
 
 @pytest.mark.parametrize("name", WORKLOADS)

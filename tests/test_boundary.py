@@ -211,6 +211,40 @@ def test_slice_host_validation(lib, S, D, sl, n_reqs, status):
     assert _call_slice(S, D, sl, n_reqs) == status
 
 
+def _call_buffer_slice(op, P, B, sl, n_reqs=1):
+    L = kvx.lib()
+    pd, bd = kvx.pool_desc(P, FAKE), kvx.buf_desc(B, FAKE)
+    x = None if sl is None else ctypes.byref(kvx.slice_desc(sl))
+    if op == "gather":
+        return L.kvx_gather_slice(ctypes.byref(pd), ctypes.byref(bd), x, FAKE, 1, FAKE, n_reqs,
+                                  None, None)
+    return L.kvx_scatter_slice(ctypes.byref(bd), ctypes.byref(pd), x, FAKE, 1, FAKE, n_reqs,
+                               None, None)
+
+
+V_ONLY = BufSpec(2, 1, 4, 64, 2, cap=1 << 16)
+
+
+@pytest.mark.parametrize("op,P,B,sl,n_reqs,status", [
+    ("gather", GOOD, V_ONLY, (0, 0, 2, 1, 0, 1, 0, 0, 4), 0, 0),      # V only, nothing to enqueue
+    ("scatter", GOOD, V_ONLY, (0, 0, 2, 0, 1, 1, 0, 0, 4), 0, 0),
+    ("gather", GOOD, V_ONLY, None, 1, -1),                           # NULL slice
+    ("scatter", GOOD, V_ONLY, None, 1, -1),
+    ("gather", GOOD, BufSpec(2, 2, 4, 64, 2, cap=1 << 16), (0, 0, 2, 1, 0, 1, 0, 0, 4), 1, -2),
+    ("gather", GOOD, V_ONLY, (0, 1, 2, 1, 0, 1, 0, 0, 4), 1, -5),   # buffer-side layer offset
+    ("scatter", GOOD, V_ONLY, (0, 0, 2, 1, 1, 1, 0, 0, 4), 1, -5),  # buffer-side kv offset
+    ("gather", GOOD, V_ONLY, (1, 0, 2, 1, 0, 1, 0, 0, 4), 1, -5),   # layers past the pool
+    ("scatter", GOOD, V_ONLY, (0, 0, 2, 0, 2, 1, 0, 0, 4), 1, -5),  # kv past the pool
+    ("gather", GOOD, BufSpec(2, 1, 2, 64, 2, cap=1 << 16), (0, 0, 2, 1, 0, 1, 3, 0, 2), 1, -5),
+    ("gather", GOOD, BufSpec(2, 1, 4, 32, 2, cap=1 << 16), (0, 0, 2, 1, 0, 1, 0, 0, 4), 1, -2),
+    ("scatter", GOOD, BufSpec(1, 1, 4, 64, 2, cap=1 << 16), (0, 0, 2, 0, 1, 1, 0, 0, 4), 1, -2),
+])
+def test_buffer_slice_host_validation(lib, op, P, B, sl, n_reqs, status):
+    assert _call_buffer_slice(op, P, B, sl, n_reqs) == status
+    if status:
+        assert kvx.kvx_last_error() != ""
+
+
 def test_layered_host_validation(lib):
     L = kvx.lib()
     sp, dp = kvx.pool_desc(BIG, FAKE), kvx.pool_desc(BIG, FAKE)

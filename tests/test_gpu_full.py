@@ -41,8 +41,12 @@ def _run(torch, wl, mem, d):
                                d["reqs"], err)
     elif st.op == "transfer":
         kvx.kvx_transfer(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"], err)
+    elif st.op == "gather" and st.slice is not None:
+        kvx.kvx_gather_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["spt"], d["reqs"], err)
     elif st.op == "gather":
         kvx.kvx_gather(mem[st.src], S, mem[st.dst], D, d["spt"], d["reqs"], err)
+    elif st.slice is not None:
+        kvx.kvx_scatter_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["dpt"], d["reqs"], err)
     else:
         kvx.kvx_scatter(mem[st.src], S, mem[st.dst], D, d["dpt"], d["reqs"], err)
     torch.cuda.synchronize()
@@ -104,4 +108,24 @@ def test_full_host_offload_onload(torch):
         old = before[l].reshape(S.N, per_page)[g.src_pt]
         new = after.reshape(S.N, per_page)[s.dst_pt]
         assert np.array_equal(old, new)
+    _free(torch, mem, dsteps)
+
+
+def test_full_host_v_only_offload_onload(torch):
+    """The host-tier pages, V only: the offload fills a V-only pinned buffer
+    and the onload writes only the V half of the fresh pages."""
+    from oracle import layer_check
+    wl, mem, dsteps = _setup(torch, "host_tier_v")
+    g, s = wl.steps
+    S, B = wl.sides["A"], wl.sides["buf"]
+    layers = sorted({0, S.L // 2, S.L - 1})
+    before = {l: layer_check.pool_layer(mem["A"], S, l) for l in layers}
+    assert _run(torch, wl, mem, dsteps[0]) == 0
+    assert _run(torch, wl, mem, dsteps[1]) == 0
+    for l in layers:
+        after = layer_check.pool_layer(mem["A"], S, l)
+        ok_g, ok_s = layer_check.gather_scatter_slice_layer(before[l], S, mem["buf"], B, after,
+                                                            g, s, l)
+        print(f"  layer {l}: V offload equal={ok_g}, V onload equal={ok_s}", flush=True)
+        assert ok_g and ok_s
     _free(torch, mem, dsteps)

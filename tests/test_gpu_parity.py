@@ -36,7 +36,7 @@ def test_tiny_workload():
 
 
 @pytest.mark.parametrize("name", ["handoff", "relayout", "mla", "host_tier", "tp_reshard",
-                                  "cow_fork", "handoff_layered", "small_requests"])
+                                  "cow_fork", "handoff_layered", "small_requests", "host_tier_v"])
 def test_small_workloads(name):
     check(get(name, small=True))
 
@@ -72,6 +72,18 @@ def test_transfer_into_pinned_host_pool(ls, ld, Ts, Td):
     wl = cases.transfer_case(ls, ld, Ts, Td, seed=Ts * 13 + Td)
     wl.host_sides = ("B",)
     check(wl)
+
+
+@pytest.mark.parametrize("k", range(len(cases.BUFFER_SLICES)))
+@pytest.mark.parametrize("ls,ld", [("LPCTHD", "LPCTHD"), ("PLCHTD", "LPCTHD"), ("LPCHTD", "PLCTHD")])
+@pytest.mark.parametrize("T", [1, 8, 64])
+def test_buffer_slices(k, ls, ld, T):
+    """A slice of one pool gathered into a buffer of exactly the slice and
+    scattered into a slice of another pool (K only, V only, K into V, a
+    tensor-parallel shard of a layer stage, a larger pool, one row)."""
+    a, b, sl, off = cases.BUFFER_SLICES[k]
+    check(cases.buffer_slice_case(ls, ld, T, a, b, sl, off, seed=k * 10 + T,
+                                  pinned=(k + T) % 2 == 1))
 
 
 def test_offset_views_into_pinned_host_memory():
