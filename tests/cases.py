@@ -195,6 +195,19 @@ def random_gs_case(seed: int) -> Workload:
     e = pick([1, 2, 4, 8])
     D = (16 // e) * pick([1, 2, 3])
     L, C, H = int(rng.integers(1, 4)), int(rng.integers(1, 3)), pick([1, 2, 3])
+    # sometimes a slice: the buffer holds (nl, nc, nh) of the pool's
+    # (L, C, H), gathered at one offset and scattered at another of a second
+    # pool of another shape
+    sliced = rng.random() < 0.3
+    if sliced:
+        L2, C2, H2 = int(rng.integers(1, 4)), int(rng.integers(1, 3)), pick([1, 2, 3, 5])
+        nl = int(rng.integers(1, min(L, L2) + 1))
+        nc = int(rng.integers(1, min(C, C2) + 1))
+        nh = int(rng.integers(1, min(H, H2) + 1))
+        g_off = [int(rng.integers(0, x - n + 1)) for x, n in ((L, nl), (C, nc), (H, nh))]
+        s_off = [int(rng.integers(0, x - n + 1)) for x, n in ((L2, nl), (C2, nc), (H2, nh))]
+    else:
+        (L2, C2, H2), (nl, nc, nh) = (L, C, H), (L, C, H)
     align = 16 // e
     ns = [0 if rng.random() < 0.1 else int(rng.integers(1, 3 * T + 6))
           for _ in range(int(rng.integers(1, 6)))]
@@ -203,12 +216,12 @@ def random_gs_case(seed: int) -> Workload:
     blocks, off = [], int(rng.integers(0, 3)) * align
     for n in ns:
         blocks.append(off)
-        off += _cdiv(L * C * n * H * D, align) * align + int(rng.integers(0, 3)) * align
-    B = BufSpec(L, C, H, D, e, cap=off)
+        off += _cdiv(nl * nc * n * nh * D, align) * align + int(rng.integers(0, 3)) * align
+    B = BufSpec(nl, nc, nh, D, e, cap=off)
     S = PoolSpec(L, C, H, D, T=T, N=sum(_cdiv(s + n, T) for n, s in zip(ns, starts)) + 2, e=e,
                  layout=layout)
-    P2 = PoolSpec(L, C, H, D, T=T, N=sum(_cdiv(s + n, T) for n, s in zip(ns, dstarts)) + 2, e=e,
-                  layout=layout)
+    P2 = PoolSpec(L2, C2, H2, D, T=T, N=sum(_cdiv(s + n, T) for n, s in zip(ns, dstarts)) + 2,
+                  e=e, layout=pick(LAYOUTS) if sliced else layout)
     perm, dperm = rng.permutation(S.N).astype(np.int32), rng.permutation(P2.N).astype(np.int32)
     g_rows, s_rows, pt, dpt = [], [], [], []
     for n, s0, d0, bo in zip(ns, starts, dstarts, blocks):
@@ -229,9 +242,12 @@ def random_gs_case(seed: int) -> Workload:
         pt[int(rng.integers(len(pt)))] = S.N
     elif damage < 0.26 and len(dpt):
         dpt[int(rng.integers(len(dpt)))] = -1
-    steps = [Step("gather", "A", "buf", pt, None, g_rows),
-             Step("scatter", "buf", "B", None, dpt, s_rows)]
-    return Workload("case", f"random gather/scatter {seed}: {layout}/T{T} ({L},{C},{H}) e{e} D{D}",
+    gsl = (g_off[0], 0, nl, g_off[1], 0, nc, g_off[2], 0, nh) if sliced else None
+    ssl = (0, s_off[0], nl, 0, s_off[1], nc, 0, s_off[2], nh) if sliced else None
+    steps = [Step("gather", "A", "buf", pt, None, g_rows, slice=gsl),
+             Step("scatter", "buf", "B", None, dpt, s_rows, slice=ssl)]
+    return Workload("case", f"random gather/scatter {seed}: {layout}/T{T} ({L},{C},{H}) e{e} D{D} "
+                    f"slices {gsl} {ssl}",
                     {"A": S, "buf": B, "B": P2}, steps, value_seed=seed, prefill_tag=seed & 0xFF,
                     host_sides=("buf",) if rng.random() < 0.3 else ())
 
