@@ -26,7 +26,6 @@ Request records are ``(n, 6)`` int64 arrays with columns
 """
 from __future__ import annotations
 
-import dataclasses
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -382,10 +381,6 @@ def get(name: str, small: bool = False) -> Workload:
             "host_tier": host_tier, "tp_reshard": tp_reshard,
             "cow_fork": cow_fork, "handoff_layered": handoff_layered,
             "small_requests": small_requests, "host_tier_v": host_tier_v}[name](small=small)
-
-
-def replace_pool(spec: PoolSpec, **kw) -> PoolSpec:
-    return dataclasses.replace(spec, **kw)
 
 
 # --------------------------------------------------------------------------

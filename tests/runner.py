@@ -5,8 +5,8 @@ from __future__ import annotations
 import numpy as np
 
 from oracle import kvx_oracle
-from paper_2606_31093_amd.workloads import (BufSpec, normal_bf16_bytes, prefill_bytes,
-                                            random_bytes, value_side)
+from paper_2606_31093_amd.workloads import (normal_bf16_bytes, prefill_bytes, random_bytes,
+                                            value_side)
 
 
 def initial_bytes(wl) -> dict:
@@ -105,6 +105,3 @@ def assert_same(got: dict, want: dict, what: str = "") -> None:
             raise AssertionError(f"{what} side {name}: {len(bad)} of {a.size} bytes differ; "
                                  f"first offsets {bad[:8].tolist()}")
 
-
-def is_buf(spec) -> bool:
-    return isinstance(spec, BufSpec)
