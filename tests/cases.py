@@ -299,3 +299,45 @@ BUFFER_SLICES = [((3, 2, 4), (3, 2, 4), (0, 0, 3, 0, 0, 2, 0, 0, 4), (0, 0, 0)),
                  ((4, 2, 8), (2, 2, 4), (2, 0, 2, 0, 0, 2, 4, 0, 4), (0, 0, 0)),   # TP shard of a stage
                  ((2, 1, 3), (3, 1, 5), (0, 0, 2, 0, 0, 1, 1, 0, 2), (1, 0, 3)),   # into a larger pool
                  ((2, 2, 2), (2, 2, 2), (1, 0, 1, 1, 0, 1, 1, 0, 1), (0, 0, 0))]   # one row per token
+
+
+def random_cow_case(seed: int) -> Workload:
+    """A seeded random copy inside one pool (copy-on-write, Sec. 4.1.4):
+    requests read pages of a shared prefix and write fresh pages of the same
+    pool; no page is both read and written, so the result is defined."""
+    rng = np.random.default_rng(40_000 + seed)
+    pick = lambda xs: xs[int(rng.integers(len(xs)))]
+    layout, T = pick(LAYOUTS), pick([1, 2, 4, 5, 8, 16])
+    e = pick([1, 2, 4])
+    D = (16 // e) * pick([1, 2])
+    L, C, H = int(rng.integers(1, 4)), int(rng.integers(1, 3)), pick([1, 2, 3])
+    spec = [(int(rng.integers(0, 2 * T)), int(rng.integers(0, 2 * T)),
+             int(rng.integers(0, 3 * T + 4))) for _ in range(int(rng.integers(1, 5)))]
+    k_read = sum(_cdiv(s0 + n, T) for s0, _d0, n in spec)
+    k_write = sum(_cdiv(d0 + n, T) for _s0, d0, n in spec)
+    P = PoolSpec(L, C, H, D, T=T, N=k_read + k_write + 3, e=e, layout=layout)
+    perm = rng.permutation(P.N).astype(np.int32)
+    reads, writes = perm[:k_read], perm[k_read:k_read + k_write]
+    src_pt, dst_pt, rows = [], [], []
+    for s0, d0, n in spec:
+        rows.append([len(src_pt), len(dst_pt), 0, s0, d0, n])
+        src_pt.extend(reads[len(src_pt): len(src_pt) + _cdiv(s0 + n, T)])
+        dst_pt.extend(writes[len(dst_pt): len(dst_pt) + _cdiv(d0 + n, T)])
+    step = Step("transfer", "A", "A", np.asarray(src_pt, np.int32), np.asarray(dst_pt, np.int32),
+                np.asarray(rows, np.int64).reshape(-1, 6))
+    return Workload("case", f"random copy-on-write {seed}: {layout}/T{T} ({L},{C},{H}) e{e} D{D}",
+                    {"A": P}, [step], value_seed=seed, prefill_tag=seed & 0xFF)
+
+
+def random_layered_case(seed: int) -> Workload:
+    """A seeded random transfer (``random_case``) moved in random layer groups."""
+    wl = random_case(1000 + seed)
+    st = wl.steps[0]
+    n_layers = st.slice[2] if st.slice is not None else wl.sides["A"].L
+    st.layer_group = int(np.random.default_rng(50_000 + seed).integers(1, max(1, n_layers) + 2))
+    wl.title += f", layer groups of {st.layer_group}"
+    return wl
+
+
+RANDOM_COW_CASES = 40
+RANDOM_LAYERED_CASES = 40

@@ -160,6 +160,18 @@ def test_random_gather_scatter(seed):
     check(cases.random_gs_case(seed))
 
 
+@pytest.mark.parametrize("seed", range(cases.RANDOM_COW_CASES))
+def test_random_copy_on_write(seed):
+    """Seeded random copies inside one pool into fresh pages."""
+    check(cases.random_cow_case(seed))
+
+
+@pytest.mark.parametrize("seed", range(cases.RANDOM_LAYERED_CASES))
+def test_random_layered(seed):
+    """Seeded random transfers moved in random layer groups."""
+    check(cases.random_layered_case(seed))
+
+
 def test_many_requests_and_empty_ones():
     spec = [((7 * i) % 13, (5 * i) % 11, (i * 37) % 90 if i % 4 else 0, None) for i in range(60)]
     check(cases.transfer_case("LPCTHD", "PLCHTD", 16, 32, seed=5, H=2, D=64, spec=spec))

@@ -149,3 +149,8 @@ def test_random_cases_are_well_formed():
         _, errs = run_oracle(wl, initial_bytes(wl))
         gs_bits.add(tuple(errs))
     assert (0, 0) in gs_bits and len(gs_bits) > 2
+    for seed in range(cases.RANDOM_COW_CASES):
+        st = cases.random_cow_case(seed).steps[0]
+        assert not set(st.src_pt.tolist()) & set(st.dst_pt.tolist())   # reads and writes disjoint
+    for seed in range(cases.RANDOM_LAYERED_CASES):
+        assert cases.random_layered_case(seed).steps[0].layer_group >= 1
