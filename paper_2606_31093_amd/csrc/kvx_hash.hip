@@ -7,11 +7,12 @@
 //
 // 1. Digests.  One wavefront per request (a grid-stride loop over
 //    requests); pages are taken 64 at a time and lane j computes c_j,
-//    issuing the loads of 64 words (a whole 256-byte page of token ids)
-//    before hashing them, so the cache lines a page shares with its
-//    neighbours are fetched while they are all in flight.  c_j goes to
+//    issuing its page's loads KVX_HASH_BATCH words at a time before hashing
+//    them.  Larger batches fetch the lines that neighbouring pages share
+//    fewer times but hold more registers, so fewer wavefronts hide load
+//    latency; 32 words (128 bytes) is the measured balance.  c_j goes to
 //    out[out_off + j], 64 pages per coalesced store.  This is where the
-//    arithmetic is: 256 bytes hashed per page.
+//    arithmetic is: 256 bytes hashed per 64-token page of int32 ids.
 //
 // 2. Chain.  One lane per request: the lane walks its request's digests in
 //    page order and overwrites each with h_j.  16 bytes hashed per page, but
