@@ -332,6 +332,25 @@ def test_thousands_of_requests():
                               extra_pages=0))
 
 
+def test_max_records():
+    """KVX_MAX_REQS (65536) records of 0-2 tokens in one call: the record scan
+    runs through 256 chunks.  Each record writes its own destination page;
+    sources are random, shared pages."""
+    rng = np.random.default_rng(65536)
+    n = 65536
+    S = PoolSpec(1, 1, 1, 8, T=4, N=512, e=2, layout="LPCTHD")
+    Dp = PoolSpec(1, 1, 1, 8, T=2, N=n, e=2, layout="LPCTHD")
+    toks = rng.integers(0, 3, size=n)
+    s0 = rng.integers(0, 3, size=n) % np.maximum(1, 5 - toks)       # s0 + toks <= 4: one page
+    src_pt = rng.integers(0, S.N, size=n).astype(np.int32)
+    dst_pt = rng.permutation(n).astype(np.int32)
+    rows = np.stack([np.arange(n), np.arange(n), np.zeros(n), s0, np.zeros(n), toks], 1)
+    wl = Workload("case", "65536 records", {"A": S, "B": Dp},
+                  [Step("transfer", "A", "B", src_pt, dst_pt, rows.astype(np.int64))],
+                  value_seed=7, prefill_tag=7)
+    check(wl)
+
+
 def test_graph_replays_match_eager():
     """The transfer captured in a HIP graph and replayed several times, with
     eager work in between, gives the eager result every time."""
