@@ -392,7 +392,7 @@ uint32_t ora_scatter_slice(const uint8_t *src, const ora_buf *B, uint8_t *dst,
  * Chained page hashes (Sec. 5.1 "Chained Paged Hashing": each page's hash
  * encodes the hash of its predecessor, so two hashes are equal only when the
  * whole prefix matches page by page).  The paper names no hash function;
- * this build's definition:
+ * the definition used here:
  *
  *   fnv(bytes, h): FNV-1a 64 (Fowler, Noll and Vo): for each byte b in
  *       order, h = (h xor b) * 0x100000001b3 mod 2^64; the empty-input state
