@@ -430,7 +430,7 @@ def hash_bench(args) -> int:
         "roofline": {"bound": "alu", "achieved": round(achieved, 2), "peak": round(HASH_PEAK_GBPS, 1),
                      "unit": "GB/s", "frac": round(achieved / HASH_PEAK_GBPS, 4),
                      "traffic": tr["traffic_bytes_per_launch"] if tr else None,
-                     "kernel": "kvx page hashes (digest + chain launches)", "bytes_per_launch": nbytes,
+                     "kernel": "kvx page hashes (digest and chain roles in one launch)", "bytes_per_launch": nbytes,
                      "kernel_ms": round(kern_ms, 4)},
         "cpu_baseline": cpu,
         "context": {"kernel_sha": kernel_sha("page_hash"),

@@ -49,6 +49,10 @@
  *   - KVX_DERR_PT_RANGE: a table index outside [0, pt_len);
  *   - KVX_DERR_BAD_REQ: a malformed request record.  The whole record is
  *     skipped.
+ *   - KVX_DERR_STALLED (kvx_page_hashes only): the chain of a group waited
+ *     longer than its bound for a digest and gave up; outputs of that group
+ *     are incomplete.  The bound is far beyond any digest time, so this
+ *     indicates a defect in the library, not in the input.
  * - The destination side is resolved before the source side, so a
  *   position bad on both sides reports only the destination bit.
  * - Source and destination may be the same pool.  Copy-on-write of shared
@@ -104,6 +108,7 @@ typedef enum kvx_status {
 #define KVX_DERR_DST_PAGE 2u
 #define KVX_DERR_PT_RANGE 4u
 #define KVX_DERR_BAD_REQ 8u
+#define KVX_DERR_STALLED 16u
 
 /* A paged pool of num_pages pages; element (l, p, c, t, h, d) lives where
  * `layout` puts it.  `base` is device memory (or device-mapped pinned host
@@ -270,9 +275,9 @@ typedef struct kvx_hash_req {
  * payload_positions records.  rec_bytes: a positive multiple of 4.
  * page_tokens: 1 .. KVX_MAX_PAGE_TOKENS.  out: out_len uint64 words,
  * 8-byte aligned; requests must not share output words, and out must not
- * overlap the payload.  The call enqueues two kernels: the first writes the
- * page digests c_j into out, the second replaces them with the chained
- * hashes, so out holds final values only once the stream has passed both.
+ * overlap the payload.  The call enqueues one kernel, which writes the page
+ * digests c_j into out and replaces each with h_j once h_{j-1} is known, so
+ * out holds final values only once the stream has passed the kernel.
  * A record whose positions or outputs fall outside the arrays, with
  * n_positions < 0 or a nonzero reserved word, is skipped (its outputs are
  * not written) and raises KVX_DERR_BAD_REQ. */

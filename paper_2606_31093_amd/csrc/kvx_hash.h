@@ -18,6 +18,7 @@ struct HashParams {
     uint64_t *out;
     int64_t out_len;
     uint32_t *err;
+    int32_t group;                // requests per workgroup in the fused kernel
 };
 
 int launch_hash(const HashParams &p, hipStream_t stream);

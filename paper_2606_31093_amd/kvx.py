@@ -28,6 +28,7 @@ DERR_SRC_PAGE = 1
 DERR_DST_PAGE = 2
 DERR_PT_RANGE = 4
 DERR_BAD_REQ = 8
+DERR_STALLED = 16
 
 STATUS = {0: "KVX_OK", -1: "KVX_ERR_NULL", -2: "KVX_ERR_SHAPE", -3: "KVX_ERR_ALIGN",
           -4: "KVX_ERR_LAYOUT", -5: "KVX_ERR_RANGE", -6: "KVX_ERR_HIP"}

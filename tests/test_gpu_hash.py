@@ -135,3 +135,62 @@ def test_random_hash_cases(torch, seed):
     got, gerr, want, werr = _both(torch, pay, rec_bytes, T, rows, out_len)
     assert gerr == werr
     assert np.array_equal(got, want)
+
+
+def _rows_for(n, T, rng, seeded=0.3):
+    rows, pos, out = [], 0, 0
+    for k in n:
+        seed_v = int(rng.integers(0, 2**63)) if rng.random() < seeded else 0
+        rows.append((pos, out, seed_v, int(k)))
+        pos += int(k)
+        out += -(-int(k) // T)
+    return rows, pos, out
+
+
+def test_more_requests_than_one_group_per_compute_unit(torch):
+    """20000 requests: 64 per group, more groups than workgroups, so each
+    workgroup takes several groups in turn and reuses its shared state."""
+    rng = np.random.default_rng(91)
+    T = 4
+    n = rng.integers(0, 3 * T + 2, size=20000)
+    rows, pos, out = _rows_for(n, T, rng)
+    pay = rng.integers(0, 2**31, size=max(pos, 1), dtype=np.int32)
+    got, gerr, want, werr = _both(torch, pay, 4, T, rows, out)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
+
+
+def test_maximum_request_count(torch):
+    """KVX_MAX_REQS (65536) records of 0-2 pages in one call."""
+    rng = np.random.default_rng(92)
+    T = 2
+    n = rng.integers(0, 2 * T + 1, size=65536)
+    rows, pos, out = _rows_for(n, T, rng)
+    pay = rng.integers(0, 2**31, size=max(pos, 1), dtype=np.int32)
+    got, gerr, want, werr = _both(torch, pay, 4, T, rows, out)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("case", ["all_empty", "equal_lengths", "one_long", "ladder"])
+def test_group_shapes(torch, case):
+    """Groups whose page counts are all zero, all equal (ties in the order
+    the pages are handed out), one long request among one-page ones, and a
+    ladder of distinct lengths."""
+    rng = np.random.default_rng(len(case))
+    T = 8
+    nreq = 700                                  # 3 requests per group on 256 compute units
+    if case == "all_empty":
+        n = np.zeros(nreq, int)
+    elif case == "equal_lengths":
+        n = np.full(nreq, 5 * T)
+    elif case == "one_long":
+        n = np.full(nreq, 1)
+        n[::97] = 3000 * T
+    else:
+        n = np.arange(nreq) % 70 * T + np.arange(nreq) % 3
+    rows, pos, out = _rows_for(n, T, rng)
+    pay = rng.integers(0, 2**31, size=max(pos, 1), dtype=np.int32)
+    got, gerr, want, werr = _both(torch, pay, 4, T, rows, out + 1)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
