@@ -194,3 +194,30 @@ def test_group_shapes(torch, case):
     got, gerr, want, werr = _both(torch, pay, 4, T, rows, out + 1)
     assert gerr == werr == 0
     assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("where", ["payload", "out", "both"])
+def test_pinned_host_payload_and_output(torch, where):
+    """Token ids and/or the output words in pinned host memory, read and
+    written over PCIe: digests arrive far more slowly, so the chain side
+    waits on them much longer than with device memory."""
+    from oracle import kvx_oracle
+    from paper_2606_31093_amd import kvx
+    rng = np.random.default_rng(len(where) + 500)
+    T = 16
+    n = rng.integers(1, 40 * T, size=300)
+    rows, pos, out_len = _rows_for(n, T, rng)
+    pay = rng.integers(0, 2**31, size=pos, dtype=np.int32)
+    want = np.zeros(out_len, np.uint64)
+    assert kvx_oracle.default().page_hashes(pay, 4, T, rows, want) == 0
+    host_pay = where in ("payload", "both")
+    host_out = where in ("out", "both")
+    p = torch.from_numpy(pay.view(np.uint8).copy())
+    p = p.pin_memory() if host_pay else p.cuda()
+    out = torch.zeros(out_len, dtype=torch.int64, pin_memory=True) if host_out else \
+        torch.zeros(out_len, dtype=torch.int64, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kvx.kvx_page_hashes(p, 4, T, kvx.device_hash_reqs(rows), out, err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    assert np.array_equal(out.cpu().numpy().view(np.uint64), want)
