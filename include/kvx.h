@@ -52,7 +52,9 @@
  *   - KVX_DERR_STALLED (kvx_page_hashes only): the chain of a group waited
  *     longer than its bound for a digest and gave up; outputs of that group
  *     are incomplete.  The bound is far beyond any digest time, so this
- *     indicates a defect in the library, not in the input.
+ *     indicates a defect in the library, not in the input.  The environment
+ *     variable KVX_HASH_IDLE_POLLS (a positive count of empty polls), read
+ *     at each call, replaces the bound; tests use it to force the case.
  * - The destination side is resolved before the source side, so a
  *   position bad on both sides reports only the destination bit.
  * - Source and destination may be the same pool.  Copy-on-write of shared

@@ -18,7 +18,8 @@ struct HashParams {
     uint64_t *out;
     int64_t out_len;
     uint32_t *err;
-    int32_t group;                // requests per workgroup in the fused kernel
+    int32_t group;                // requests per workgroup
+    uint64_t idle_limit;          // empty polls in a row before the chain gives up
 };
 
 int launch_hash(const HashParams &p, hipStream_t stream);

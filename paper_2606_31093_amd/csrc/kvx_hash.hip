@@ -31,6 +31,8 @@
 // out[] holds digests until the chain has passed them: callers see it only
 // after the stream has passed the kernel.
 
+#include <stdlib.h>
+
 #include "kvx_hash.h"
 
 namespace kvx {
@@ -251,9 +253,7 @@ __global__ void __launch_bounds__(kWave * (1 + kDW)) kvx_page_hash_kernel(HashPa
 #pragma unroll
             for (int u = 0; u < B; ++u) cn[u] = 0;
             uint64_t idle = 0;
-            // consecutive empty polls allowed: far more than one page's digest
-            // takes even with the payload in host memory
-            const uint64_t idle_limit = (1ull << 22) + 64ull * (uint64_t)p.T * (uint64_t)p.rec_bytes;
+            const uint64_t idle_limit = p.idle_limit;
             while (__any(j < pages)) {
                 uint64_t lim = kAllDone;
 #pragma unroll
@@ -322,6 +322,15 @@ int launch_hash(const HashParams &p0, hipStream_t stream) {
     e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
     if (e != hipSuccess) return e;
     HashParams p = p0;
+    // Empty polls in a row the chain allows: far more than one page's digest
+    // takes, even with the payload in host memory.  KVX_HASH_IDLE_POLLS
+    // overrides it (tests use a tiny value to see the chain give up cleanly).
+    p.idle_limit = (1ull << 22) + 64ull * (uint64_t)p.T * (uint64_t)p.rec_bytes;
+    if (const char *env = getenv("KVX_HASH_IDLE_POLLS")) {
+        char *end = nullptr;
+        const unsigned long long v = strtoull(env, &end, 10);
+        if (end != env && *end == '\0' && v > 0) p.idle_limit = v;
+    }
     // one group per compute unit, each of at most 64 requests
     const int32_t group = (p.n_reqs + cus - 1) / cus;
     p.group = group < 1 ? 1 : group > kSlots ? kSlots : group;

@@ -221,3 +221,22 @@ def test_pinned_host_payload_and_output(torch, where):
     torch.cuda.synchronize()
     assert int(err.item()) == 0
     assert np.array_equal(out.cpu().numpy().view(np.uint64), want)
+
+
+def test_chain_wait_gives_up_cleanly(torch, monkeypatch):
+    """With the chain's wait bound forced down to one empty poll, the chain
+    stops before the first digests exist: the kernel still finishes, raises
+    KVX_DERR_STALLED and leaves the outputs incomplete.  The next call, with
+    the normal bound, is exact again."""
+    from paper_2606_31093_amd import kvx
+    wl = W.page_hash(small=True)
+    pay = W.hash_payload(wl)
+    monkeypatch.setenv("KVX_HASH_IDLE_POLLS", "1")
+    got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
+    assert werr == 0
+    assert gerr & kvx.DERR_STALLED
+    assert not np.array_equal(got, want)
+    monkeypatch.delenv("KVX_HASH_IDLE_POLLS")
+    got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
+    assert gerr == werr == 0
+    assert np.array_equal(got, want)
