@@ -240,3 +240,34 @@ def test_chain_wait_gives_up_cleanly(torch, monkeypatch):
     got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
     assert gerr == werr == 0
     assert np.array_equal(got, want)
+
+
+def test_graph_replays_match_eager(torch):
+    """The hash kernel captured in a HIP graph and replayed several times,
+    with the output cleared eagerly in between, gives the oracle's words
+    every time."""
+    from paper_2606_31093_amd import kvx
+    from oracle import kvx_oracle
+    wl = W.page_hash(small=True)
+    pay = W.hash_payload(wl)
+    want = np.zeros(wl.out_len, np.uint64)
+    assert kvx_oracle.default().page_hashes(pay, wl.rec_bytes, wl.T, wl.rows, want) == 0
+    p = torch.from_numpy(pay.view(np.uint8).copy()).cuda()
+    reqs = kvx.device_hash_reqs(wl.rows)
+    out = torch.zeros(wl.out_len, dtype=torch.int64, device="cuda")
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        kvx.kvx_page_hashes(p, wl.rec_bytes, wl.T, reqs, out, err, stream=s)      # warm up
+    torch.cuda.current_stream().wait_stream(s)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        kvx.kvx_page_hashes(p, wl.rec_bytes, wl.T, reqs, out, err)
+    for _ in range(3):
+        out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert int(err.item()) == 0
+        assert np.array_equal(out.cpu().numpy().view(np.uint64), want)

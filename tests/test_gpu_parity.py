@@ -380,6 +380,45 @@ def test_graph_replays_match_eager():
         assert np.array_equal(b.cpu().numpy(), want["B"])
 
 
+def test_concurrent_calls_on_three_streams():
+    """Two transfers out of the same source pool into two destination pools
+    and a page-hash call, each on its own stream and in flight together:
+    the library keeps no state between calls, so each result equals the
+    oracle's for that call alone."""
+    import torch
+    from oracle import kvx_oracle
+    from paper_2606_31093_amd import kvx
+    from paper_2606_31093_amd import workloads as W
+    wl = get("handoff", small=True)
+    st = wl.steps[0]
+    init = initial_bytes(wl)
+    want, _ = run_oracle(wl, init)
+    a = torch.from_numpy(init["A"]).cuda()
+    b1 = torch.from_numpy(init["B"]).cuda()
+    b2 = torch.from_numpy(init["B"]).cuda()
+    spt, dpt, reqs = kvx.device_table(st.src_pt), kvx.device_table(st.dst_pt), kvx.device_reqs(st.reqs)
+    hw = W.page_hash(small=True)
+    pay = W.hash_payload(hw)
+    hwant = np.zeros(hw.out_len, np.uint64)
+    assert kvx_oracle.default().page_hashes(pay, hw.rec_bytes, hw.T, hw.rows, hwant) == 0
+    tpay = torch.from_numpy(pay.view(np.uint8).copy()).cuda()
+    hreqs = kvx.device_hash_reqs(hw.rows)
+    hout = torch.zeros(hw.out_len, dtype=torch.int64, device="cuda")
+    errs = torch.zeros(3, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    for rep in range(3):
+        kvx.kvx_transfer(a, wl.sides["A"], b1, wl.sides["B"], spt, dpt, reqs, errs[0:1], stream=streams[0])
+        kvx.kvx_transfer(a, wl.sides["A"], b2, wl.sides["B"], spt, dpt, reqs, errs[1:2], stream=streams[1])
+        kvx.kvx_page_hashes(tpay, hw.rec_bytes, hw.T, hreqs, hout, errs[2:3], stream=streams[2])
+    torch.cuda.synchronize()
+    assert errs.cpu().tolist() == [0, 0, 0]
+    assert np.array_equal(b1.cpu().numpy(), want["B"])
+    assert np.array_equal(b2.cpu().numpy(), want["B"])
+    assert np.array_equal(a.cpu().numpy(), init["A"])
+    assert np.array_equal(hout.cpu().numpy().view(np.uint64), hwant)
+
+
 # ---------------------------------------------------------------------------
 # error behaviour
 # ---------------------------------------------------------------------------
