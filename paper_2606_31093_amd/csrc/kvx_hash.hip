@@ -111,7 +111,7 @@ constexpr uint64_t kAllDone = ~0ull;
 // m[k-1] <= j < m[k], so item q falls in the segment k with
 // base[k] <= q < base[k+1] and each segment is a (page, position) grid.
 struct GroupLds {
-    int32_t raw[kSlots];       // page counts by slot
+    int64_t key[kSlots];       // (page count, slot) by slot, for the sort
     int32_t m[kSlots];         // page counts, ascending
     int32_t perm[kSlots];      // ascending position -> slot
     int32_t npos[kSlots];      // n_positions by slot
@@ -150,19 +150,17 @@ __global__ void __launch_bounds__(kWave * (1 + kDW)) kvx_page_hash_kernel(HashPa
                     atomicOr(p.err, KVX_DERR_BAD_REQ);
                 }
             }
-            s.raw[lane] = pages;
+            s.key[lane] = ((int64_t)pages << 6) | lane;
             s.npos[lane] = npos;
             s.pay[lane] = pay;
             s.outo[lane] = outo;
         }
         __syncthreads();
         if (wave == 0) {
-            // ascending rank, ties broken by slot
-#pragma unroll 8
-            for (int t = 0; t < kSlots; ++t) {
-                const int32_t o = s.raw[t];
-                pos += (o < pages) || (o == pages && t < lane);
-            }
+            // ascending rank of the unique key (pages, slot)
+            const int64_t key = ((int64_t)pages << 6) | lane;
+#pragma unroll
+            for (int t = 0; t < kSlots; ++t) pos += s.key[t] < key;
             s.m[pos] = pages;
             s.perm[pos] = lane;
         }
