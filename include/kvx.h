@@ -31,6 +31,9 @@
  * - Page tables, request records and the error word must be readable and
  *   writable by the device: device memory, or pinned host memory mapped for
  *   the device.
+ * - Device memory must belong to the current device (hipGetDevice); memory
+ *   of another GPU is refused with KVX_ERR_RANGE.  Kernels run on the
+ *   current device.
  * - Descriptors are read on the host during the call.
  *
  * Synchrony.

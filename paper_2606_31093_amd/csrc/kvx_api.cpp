@@ -102,6 +102,17 @@ int device_view(const void *ptr, const char *name, void **dev_ptr, bool *is_host
         return fail(KVX_ERR_RANGE, "%s (%p) is not memory the GPU can address (%s)", name, ptr,
                     hipGetErrorString(e));
     }
+    if (attr.type == hipMemoryTypeDevice) {
+        // Device memory of another GPU would fault the kernel unless peer
+        // access happened to be enabled; this library runs on one GPU.
+        int cur = 0;
+        const hipError_t ge = hipGetDevice(&cur);
+        if (ge != hipSuccess)
+            return fail(KVX_ERR_HIP, "hipGetDevice failed: %s", hipGetErrorString(ge));
+        if (attr.device != cur)
+            return fail(KVX_ERR_RANGE, "%s (%p) is memory of device %d, but the current device is %d",
+                        name, ptr, attr.device, cur);
+    }
     if (attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged ||
         attr.type == hipMemoryTypeUnified) {
         *dev_ptr = const_cast<void *>(ptr);
