@@ -117,7 +117,9 @@ typedef enum kvx_status {
 
 /* A paged pool of num_pages pages; element (l, p, c, t, h, d) lives where
  * `layout` puts it.  `base` is device memory (or device-mapped pinned host
- * memory), 16-byte aligned. */
+ * memory), 16-byte aligned, and must hold kvx_pool_bytes(pool) bytes: the
+ * library cannot see allocation sizes, so a smaller allocation is the
+ * caller's error and the kernel may fault on it. */
 typedef struct kvx_pool {
     void *base;
     int32_t num_layers;  /* L >= 1 */
@@ -132,7 +134,8 @@ typedef struct kvx_pool {
 
 /* A flat buffer of per-request blocks [layer][kv][token][head][dim] (the
  * flat serialization used by host tiers).  `base` is device memory or
- * device-mapped pinned host memory, 16-byte aligned. */
+ * device-mapped pinned host memory, 16-byte aligned, and must hold
+ * capacity_elems elements (the caller's responsibility, as for a pool). */
 typedef struct kvx_buf {
     void *base;
     int32_t num_layers, num_kv, num_heads, head_dim, elem_bytes;
