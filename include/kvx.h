@@ -135,7 +135,9 @@ typedef struct kvx_pool {
 /* A flat buffer of per-request blocks [layer][kv][token][head][dim] (the
  * flat serialization used by host tiers).  `base` is device memory or
  * device-mapped pinned host memory, 16-byte aligned, and must hold
- * capacity_elems elements (the caller's responsibility, as for a pool). */
+ * capacity_elems elements (the caller's responsibility, as for a pool).
+ * With capacity_elems == 0 `base` may be NULL: only records of 0 tokens at
+ * offset 0 then fit, and any other record raises KVX_DERR_BAD_REQ. */
 typedef struct kvx_buf {
     void *base;
     int32_t num_layers, num_kv, num_heads, head_dim, elem_bytes;

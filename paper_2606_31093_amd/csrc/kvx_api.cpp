@@ -191,7 +191,8 @@ int check_buf(const kvx_buf *b, const char *name, Shape &s) {
     int st = check_shape(name, s);
     if (st) return st;
     if (b->reserved != 0) return fail(KVX_ERR_RANGE, "%s: reserved field must be 0", name);
-    if (!b->base) return fail(KVX_ERR_NULL, "%s: base is NULL", name);
+    // An empty buffer may have no memory at all: no record can then address it.
+    if (!b->base && b->capacity_elems != 0) return fail(KVX_ERR_NULL, "%s: base is NULL", name);
     if (!aligned16(b->base)) return fail(KVX_ERR_ALIGN, "%s: base %p is not 16-byte aligned", name, b->base);
     if (b->capacity_elems < 0 || mul_checked(b->capacity_elems, b->elem_bytes) < 0)
         return fail(KVX_ERR_RANGE, "%s: capacity_elems out of range", name);
@@ -231,8 +232,9 @@ int view_all(const void *src, const void *dst, const int32_t *src_pt, int64_t sr
              Views &v) {
     int st;
     void *d = nullptr;
-    if ((st = device_view(src, "src base", &v.src))) return st;
-    if ((st = device_view(dst, "dst base", &v.dst, &v.dst_host))) return st;
+    // A NULL base here is an empty buffer (pools are never NULL): nothing to view.
+    if (src && (st = device_view(src, "src base", &v.src))) return st;
+    if (dst && (st = device_view(dst, "dst base", &v.dst, &v.dst_host))) return st;
     if (src_pt_len > 0) {
         if ((st = device_view(src_pt, "src_pt", &d))) return st;
         v.src_pt = static_cast<const int32_t *>(d);

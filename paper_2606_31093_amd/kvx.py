@@ -96,6 +96,12 @@ def lib() -> ctypes.CDLL:
         if not os.path.exists(path):
             raise RuntimeError(f"libkvx is not built ({path} missing); run "
                                "python -m paper_2606_31093_amd.build_lib")
+        # PyTorch ships its own HIP runtime.  Loaded first, it is the one
+        # libkvx binds to (same soname), so the library and torch share one
+        # runtime: the one that owns the tensors and streams passed in.
+        # Loading libkvx first would bring a second HIP and HSA runtime into
+        # the process, and one of them then finds no device.
+        import torch  # noqa: F401
         L = ctypes.CDLL(path)
         vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
         pp, bp = ctypes.POINTER(Pool), ctypes.POINTER(Buf)

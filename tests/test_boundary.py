@@ -379,3 +379,40 @@ def test_binding_rejects_wrong_table_and_error_word_types():
         kvx.kvx_page_hashes(torch.zeros(16, dtype=torch.uint8), 4, 4,
                             torch.zeros(32, dtype=torch.uint8), torch.zeros(1, dtype=torch.int64),
                             dev_err=torch.zeros(1, dtype=torch.float32))
+
+
+def test_binding_shares_torchs_hip_runtime():
+    """Loading the library through the binding, in a fresh process that has
+    not imported torch, maps exactly one HIP runtime and one HSA runtime:
+    the ones torch ships, which own the tensors and streams the calls take."""
+    import subprocess
+    import sys
+    code = (
+        "import sys; sys.path.insert(0, %r)\n"
+        "from paper_2606_31093_amd import kvx\n"
+        "kvx.lib()\n"
+        "m = sorted({l.split()[-1] for l in open('/proc/self/maps')\n"
+        "            if 'libamdhip64' in l or 'libhsa-runtime64' in l})\n"
+        "print('\\n'.join(m))\n" % ROOT)
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr
+    maps = out.stdout.split()
+    hip = [m for m in maps if "libamdhip64" in m]
+    hsa = [m for m in maps if "libhsa-runtime64" in m]
+    assert len(hip) == 1 and len(hsa) == 1, maps
+    import torch
+    torch_lib = os.path.dirname(torch.__file__)
+    assert hip[0].startswith(torch_lib) or not os.path.exists(os.path.join(torch_lib, "lib", "libamdhip64.so")), maps
+
+
+def test_empty_buffer_may_have_no_memory(lib):
+    """A buffer of capacity 0 may have a NULL base (a zero-size tensor has
+    no memory); a buffer with capacity must have memory."""
+    L = kvx.lib()
+    pd = kvx.pool_desc(GOOD, FAKE)
+    empty = kvx.buf_desc(BufSpec(GOOD.L, GOOD.C, GOOD.H, GOOD.D, GOOD.e, cap=0), 0)
+    assert L.kvx_gather(ctypes.byref(pd), ctypes.byref(empty), FAKE, 1, FAKE, 0, None, None) == 0
+    assert L.kvx_scatter(ctypes.byref(empty), ctypes.byref(pd), FAKE, 1, FAKE, 0, None, None) == 0
+    full = kvx.buf_desc(BufSpec(GOOD.L, GOOD.C, GOOD.H, GOOD.D, GOOD.e, cap=1 << 10), 0)
+    assert L.kvx_gather(ctypes.byref(pd), ctypes.byref(full), FAKE, 1, FAKE, 0, None, None) == -1
+    assert "base is NULL" in kvx.kvx_last_error()

@@ -380,6 +380,25 @@ def test_graph_replays_match_eager():
         assert np.array_equal(b.cpu().numpy(), want["B"])
 
 
+@pytest.mark.parametrize("pinned", [False, True], ids=["device", "pinned_host"])
+def test_empty_buffer_without_memory(pinned):
+    """A gather into and a scatter out of a buffer of capacity 0, which a
+    zero-size tensor gives a NULL base: records of 0 tokens copy nothing and
+    raise nothing, a record of 3 tokens raises KVX_DERR_BAD_REQ, and no pool
+    byte changes."""
+    S = PoolSpec(2, 2, 2, 16, T=4, N=6, e=2, layout="LPCHTD")
+    B = BufSpec(2, 2, 2, 16, 2, cap=0)
+    pt = np.array([3, 1, 4, 0], np.int32)
+    g_rows = np.array([[0, 0, 0, 0, 0, 0], [1, 0, 0, 2, 0, 0], [2, 0, 0, 1, 0, 3]], np.int64)
+    s_rows = np.array([[0, 0, 0, 0, 0, 0], [0, 1, 0, 0, 3, 0], [0, 2, 0, 0, 1, 3]], np.int64)
+    wl = Workload("case", "empty buffer", {"A": S, "buf": B, "B": S},
+                  [Step("gather", "A", "buf", pt, None, g_rows),
+                   Step("scatter", "buf", "B", None, pt, s_rows)],
+                  value_seed=5, prefill_tag=7, host_sides=("buf",) if pinned else ())
+    _, gerr = check(wl)
+    assert gerr == [8, 8]          # the 3-token record, in the gather and in the scatter
+
+
 def test_concurrent_calls_on_three_streams():
     """Two transfers out of the same source pool into two destination pools
     and a page-hash call, each on its own stream and in flight together:
