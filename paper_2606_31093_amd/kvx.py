@@ -209,6 +209,8 @@ def _n_reqs(reqs) -> int:
     nbytes = reqs.numel() * reqs.element_size()
     if nbytes % REQ_DTYPE.itemsize:
         raise ValueError("reqs must hold whole 40-byte kvx_req records")
+    if not reqs.is_contiguous():
+        raise ValueError("reqs must be contiguous")
     return nbytes // REQ_DTYPE.itemsize
 
 
@@ -377,6 +379,8 @@ def kvx_page_hashes(payload, rec_bytes, page_tokens, reqs, out, dev_err=None, st
     rb = reqs.numel() * reqs.element_size()
     if rb % HASH_REQ_DTYPE.itemsize:
         raise ValueError("reqs must hold whole 32-byte kvx_hash_req records")
+    if not reqs.is_contiguous():
+        raise ValueError("reqs must be contiguous")
     _check(lib().kvx_page_hashes(_ptr(payload), nbytes // rec_bytes, int(rec_bytes),
                                  int(page_tokens), _ptr(reqs), rb // HASH_REQ_DTYPE.itemsize,
                                  _ptr(out), out.numel(), _ptr(dev_err), _stream(stream)))

@@ -379,6 +379,12 @@ def test_binding_rejects_wrong_table_and_error_word_types():
         kvx.kvx_page_hashes(torch.zeros(16, dtype=torch.uint8), 4, 4,
                             torch.zeros(32, dtype=torch.uint8), torch.zeros(1, dtype=torch.int64),
                             dev_err=torch.zeros(1, dtype=torch.float32))
+    strided = torch.zeros(80, dtype=torch.uint8)[::2]          # 40 bytes, but every other one
+    with pytest.raises(ValueError, match="contiguous"):
+        kvx.kvx_transfer(a, P, a, P, t32, t32, strided)
+    with pytest.raises(ValueError, match="contiguous"):
+        kvx.kvx_page_hashes(torch.zeros(16, dtype=torch.uint8), 4, 4,
+                            torch.zeros(64, dtype=torch.uint8)[::2], torch.zeros(1, dtype=torch.int64))
 
 
 def test_binding_shares_torchs_hip_runtime():
