@@ -182,6 +182,50 @@ def random_case(seed: int) -> Workload:
 RANDOM_CASES = 200
 
 
+def random_medium_case(seed: int) -> Workload:
+    """A seeded random transfer of medium size: 100-900 requests (several
+    256-record chunks of the kernel's record scan, many tiles per
+    workgroup), random layouts and page sizes on each side, requests that
+    reread earlier source pages, and sometimes a damaged destination id."""
+    rng = np.random.default_rng(90_000 + seed)
+    pick = lambda xs: xs[int(rng.integers(len(xs)))]
+    ls, ld = pick(LAYOUTS), pick(LAYOUTS)
+    Ts, Td = pick([1, 4, 8, 16, 64, 128]), pick([2, 8, 16, 32, 64, 256])
+    e = pick([2, 4])
+    D = (16 // e) * pick([2, 4, 8])
+    L, C, H = int(rng.integers(1, 5)), int(rng.integers(1, 3)), pick([1, 2, 4])
+    nreq = int(rng.integers(100, 900))
+    spec = []
+    for r in range(nreq):
+        n = 0 if rng.random() < 0.05 else int(rng.integers(1, 3 * max(Ts, Td) + 40))
+        share = int(rng.integers(0, r)) if r and rng.random() < 0.1 else None
+        spec.append((int(rng.integers(0, 2 * Ts)), int(rng.integers(0, 2 * Td)), n, share))
+    ks = [_cdiv(s0 + n, Ts) for s0, _d0, n, share in spec if share is None]
+    kd = [_cdiv(d0 + n, Td) for _s0, d0, n, _share in spec]
+    S = PoolSpec(L, C, H, D, T=Ts, N=sum(ks) + 3, e=e, layout=ls)
+    Dp = PoolSpec(L, C, H, D, T=Td, N=sum(kd) + 3, e=e, layout=ld)
+    sperm, dperm = rng.permutation(S.N).astype(np.int32), rng.permutation(Dp.N).astype(np.int32)
+    src_pt, dst_pt, rows, src_offs = [], [], [], []
+    for s0, d0, n, share in spec:
+        k_s, k_d = _cdiv(s0 + n, Ts), _cdiv(d0 + n, Td)
+        so = src_offs[share] if share is not None else len(src_pt)
+        if share is None:
+            src_pt.extend(sperm[len(src_pt): len(src_pt) + k_s])
+        src_offs.append(so)
+        rows.append([so, len(dst_pt), 0, s0, d0, n])
+        dst_pt.extend(dperm[len(dst_pt): len(dst_pt) + k_d])
+    src_pt, dst_pt = np.asarray(src_pt, np.int32), np.asarray(dst_pt, np.int32)
+    if rng.random() < 0.2 and len(dst_pt):
+        dst_pt[int(rng.integers(len(dst_pt)))] = -1
+    step = Step("transfer", "A", "B", src_pt, dst_pt, np.asarray(rows, np.int64).reshape(-1, 6))
+    return Workload("case", f"medium {seed}: {ls}/T{Ts} -> {ld}/T{Td} ({L},{C},{H}) e{e} D{D}, "
+                    f"{nreq} requests", {"A": S, "B": Dp}, [step], value_seed=seed,
+                    prefill_tag=seed & 0xFF)
+
+
+RANDOM_MEDIUM_CASES = 24
+
+
 def random_gs_case(seed: int) -> Workload:
     """A seeded random gather (pool -> flat buffer) and scatter (buffer ->
     a second pool): random layout, page size, shape and element width, 1-5

@@ -153,6 +153,13 @@ def test_random_cases(seed):
     check(cases.random_case(seed))
 
 
+@pytest.mark.parametrize("seed", range(cases.RANDOM_MEDIUM_CASES))
+def test_random_medium_transfers(seed):
+    """Seeded random transfers of 100-900 requests: several record chunks,
+    many tiles per workgroup, random layouts and page sizes."""
+    check(cases.random_medium_case(seed))
+
+
 @pytest.mark.parametrize("seed", range(cases.RANDOM_GS_CASES))
 def test_random_gather_scatter(seed):
     """Seeded random gathers into a flat buffer (device or pinned host) and
