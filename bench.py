@@ -7,9 +7,14 @@ role handoff:
 - 36 layers x 8 KV heads x 128 head_dim, bf16;
 - 4096 x 64-token pools on both sides, layout [layer][page][kv][token][head][dim];
 - 32 requests with lengths uniform in [1024, 8192] on random page tables.
-A step is one fused kvx_transfer of all 32 requests.  ``--workload
-relayout|mla|host_tier|tp_reshard`` selects the relayout, MLA
-partial-prefix, host-tier and tensor-parallel reshard workloads.
+A step is one fused kvx_transfer of all 32 requests.  ``--workload``
+selects the others: relayout (16-token token-major pages into 64-token
+head-major ones), mla (partial-prefix copy of MLA latents), host_tier
+(offload to pinned host memory and onload into fresh pages), tp_reshard
+(a head range into a narrower pool), cow_fork (copy-on-write inside one
+pool), handoff_layered (the handoff in 4-layer groups with an event each),
+small_requests (16384 requests of 1-4 tokens), host_tier_v (the host tier
+for the V half only) and page_hash (chained page hashes of token ids).
 
 GB/s counts algorithmic bytes, GB = 1e9: every copied token position is read
 once and written once, 2 * tokens * L*C*H*D*e per step.
