@@ -406,6 +406,51 @@ def test_empty_buffer_without_memory(pinned):
     assert gerr == [8, 8]          # the 3-token record, in the gather and in the scatter
 
 
+def test_calls_from_four_host_threads():
+    """Four host threads, each with its own stream and destination pool,
+    call the library 25 times at once (ctypes releases the GIL): every
+    destination equals the oracle's, and every thread's error word and last
+    error message stay its own."""
+    import threading
+    import torch
+    from paper_2606_31093_amd import kvx
+    wl = get("handoff", small=True)
+    st = wl.steps[0]
+    init = initial_bytes(wl)
+    want, _ = run_oracle(wl, init)
+    a = torch.from_numpy(init["A"]).cuda()
+    spt, dpt, reqs = kvx.device_table(st.src_pt), kvx.device_table(st.dst_pt), kvx.device_reqs(st.reqs)
+    outs = [torch.from_numpy(init["B"]).cuda() for _ in range(4)]
+    errs = torch.zeros(4, dtype=torch.int32, device="cuda")
+    torch.cuda.synchronize()
+    failures = []
+
+    def work(t):
+        try:
+            s = torch.cuda.Stream()
+            for _ in range(25):
+                kvx.kvx_transfer(a, wl.sides["A"], outs[t], wl.sides["B"], spt, dpt, reqs,
+                                 errs[t:t + 1], stream=s)
+            with pytest.raises(kvx.KvxError):           # a host error on this thread only
+                kvx.kvx_transfer(a, wl.sides["A"], outs[t], wl.sides["B"], spt, dpt,
+                                 torch.zeros(40, dtype=torch.uint8), stream=s)
+            assert "reqs" in kvx.kvx_last_error()       # this thread's message
+            s.synchronize()
+        except Exception as e:                          # reported on the main thread
+            failures.append(repr(e))
+
+    threads = [threading.Thread(target=work, args=(t,)) for t in range(4)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join()
+    torch.cuda.synchronize()
+    assert not failures, failures
+    assert errs.cpu().tolist() == [0, 0, 0, 0]
+    for o in outs:
+        assert np.array_equal(o.cpu().numpy(), want["B"])
+
+
 def test_concurrent_calls_on_three_streams():
     """Two transfers out of the same source pool into two destination pools
     and a page-hash call, each on its own stream and in flight together:
