@@ -3,6 +3,8 @@ seconds: the tiny workload, shrunken versions of the four large ones, every
 layout pair and page-size pair, every element width, pinned host buffers,
 tiles spanning more source pages than a wavefront has lanes, and the
 documented error behaviour."""
+import zlib
+
 import numpy as np
 import pytest
 
@@ -44,7 +46,9 @@ def test_small_workloads(name):
 @pytest.mark.parametrize("ls,ld,Ts,Td", list(cases.layout_matrix()),
                          ids=lambda v: str(v))
 def test_layout_matrix(ls, ld, Ts, Td):
-    check(cases.transfer_case(ls, ld, Ts, Td, seed=hash((ls, ld, Ts, Td)) & 0xFFFF))
+    # a seed fixed by the case itself (Python salts str hashes per process)
+    seed = zlib.crc32(repr((ls, ld, Ts, Td)).encode()) & 0xFFFF
+    check(cases.transfer_case(ls, ld, Ts, Td, seed=seed))
 
 
 @pytest.mark.parametrize("e,D,C,H", [(1, 16, 2, 3), (2, 8, 2, 3), (4, 4, 1, 5), (8, 2, 2, 1),
