@@ -28,9 +28,17 @@
  *   stream.
  * - The library allocates no device or host memory and keeps no state
  *   between calls other than a thread-local error message.
- * - Page tables, request records and the error word must be readable and
- *   writable by the device: device memory, or pinned host memory mapped for
- *   the device.
+ * - Page tables and request records must be readable by the device: device
+ *   memory, or pinned host memory mapped for the device.
+ * - The error word must be device memory.  Bits are OR-ed into it with
+ *   device atomics, which pinned host memory does not support on every
+ *   platform; a host error word is refused with KVX_ERR_RANGE.
+ * - Every pointer must lie in an allocation that holds the bytes the call
+ *   may touch from it: kvx_pool_bytes(pool) for a pool, capacity_elems
+ *   elements for a buffer, pt_len entries for a page table, n_reqs records,
+ *   4 bytes for the error word.  Where the HIP runtime reports the
+ *   allocation around a pointer (every device allocation), a shorter one
+ *   is refused with KVX_ERR_RANGE before anything is enqueued.
  * - Device memory must belong to the current device (hipGetDevice); memory
  *   of another GPU is refused with KVX_ERR_RANGE.  Kernels run on the
  *   current device.
@@ -46,7 +54,7 @@
  * - A call returns KVX_OK or a negative kvx_status, with nothing enqueued.
  *   kvx_last_error() then names the failing check.
  * - Problems that only the device can see skip the affected elements and
- *   OR bits into *dev_err (when non-NULL):
+ *   OR bits into *dev_err (when non-NULL; kvx_page_hashes requires it):
  *   - KVX_DERR_SRC_PAGE / KVX_DERR_DST_PAGE: a page id outside
  *     [0, num_pages);
  *   - KVX_DERR_PT_RANGE: a table index outside [0, pt_len);
@@ -55,9 +63,9 @@
  *   - KVX_DERR_STALLED (kvx_page_hashes only): the chain of a group waited
  *     longer than its bound for a digest and gave up; outputs of that group
  *     are incomplete.  The bound is far beyond any digest time, so this
- *     indicates a defect in the library, not in the input.  The environment
- *     variable KVX_HASH_IDLE_POLLS (a positive count of empty polls), read
- *     at each call, replaces the bound; tests use it to force the case.
+ *     indicates a defect in the library, not in the input.  A build with
+ *     the macro KVX_HASH_IDLE_POLLS defined uses that many empty polls as
+ *     the bound instead; the test build sets 1 to force the case.
  * - The destination side is resolved before the source side, so a
  *   position bad on both sides reports only the destination bit.
  * - Source and destination may be the same pool.  Copy-on-write of shared
@@ -117,9 +125,9 @@ typedef enum kvx_status {
 
 /* A paged pool of num_pages pages; element (l, p, c, t, h, d) lives where
  * `layout` puts it.  `base` is device memory (or device-mapped pinned host
- * memory), 16-byte aligned, and must hold kvx_pool_bytes(pool) bytes: the
- * library cannot see allocation sizes, so a smaller allocation is the
- * caller's error and the kernel may fault on it. */
+ * memory), 16-byte aligned, and must hold kvx_pool_bytes(pool) bytes (a
+ * smaller allocation is refused where the runtime reports its size, see
+ * Ownership above). */
 typedef struct kvx_pool {
     void *base;
     int32_t num_layers;  /* L >= 1 */
@@ -135,7 +143,7 @@ typedef struct kvx_pool {
 /* A flat buffer of per-request blocks [layer][kv][token][head][dim] (the
  * flat serialization used by host tiers).  `base` is device memory or
  * device-mapped pinned host memory, 16-byte aligned, and must hold
- * capacity_elems elements (the caller's responsibility, as for a pool).
+ * capacity_elems elements (checked as for a pool).
  * With capacity_elems == 0 `base` may be NULL: only records of 0 tokens at
  * offset 0 then fit, and any other record raises KVX_DERR_BAD_REQ. */
 typedef struct kvx_buf {
@@ -290,7 +298,9 @@ typedef struct kvx_hash_req {
  * out holds final values only once the stream has passed the kernel.
  * A record whose positions or outputs fall outside the arrays, with
  * n_positions < 0 or a nonzero reserved word, is skipped (its outputs are
- * not written) and raises KVX_DERR_BAD_REQ. */
+ * not written) and raises KVX_DERR_BAD_REQ.
+ * dev_err is required (KVX_ERR_NULL when NULL): KVX_DERR_STALLED is the
+ * only sign that a group's outputs were left incomplete. */
 int kvx_page_hashes(const void *payload, int64_t payload_positions, int32_t rec_bytes,
                     int32_t page_tokens, const kvx_hash_req *reqs, int32_t n_reqs,
                     uint64_t *out, int64_t out_len, uint32_t *dev_err, void *stream);

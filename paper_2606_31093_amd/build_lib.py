@@ -15,6 +15,10 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libkvx.so")
+# A test build whose hash chain gives up after one empty poll (the bound is a
+# compile-time option, so the product library has no switch for it).
+STALL_TEST_LIBRARY = os.path.join(PKG, "libkvx_test_stall.so")
+STALL_TEST_DEFINES = ("KVX_HASH_IDLE_POLLS=1",)
 SOURCES = [os.path.join(CSRC, "kvx_kernels.hip"), os.path.join(CSRC, "kvx_hash.hip"),
            os.path.join(CSRC, "kvx_api.cpp")]
 HEADERS = [os.path.join(INCLUDE, "kvx.h"), os.path.join(CSRC, "kvx_internal.h"),
@@ -53,6 +57,11 @@ def is_stale(output: str = LIBRARY) -> bool:
         return True
     t = os.path.getmtime(output)
     return any(os.path.getmtime(s) > t for s in SOURCES + HEADERS)
+
+
+def build_all() -> list:
+    """The library and its test build."""
+    return [build(), build(STALL_TEST_LIBRARY, STALL_TEST_DEFINES)]
 
 
 if __name__ == "__main__":

@@ -92,9 +92,12 @@ int same_shape(const Shape &a, const Shape &b) {
 }
 
 // The device must be able to address `ptr` (device memory or mapped pinned
-// host memory).  On success *dev_ptr is the address kernels use and
-// *is_host (if given) tells whether it is host memory.
-int device_view(const void *ptr, const char *name, void **dev_ptr, bool *is_host = nullptr) {
+// host memory), and the allocation it points into must hold the `need`
+// bytes from `ptr` on that the call may touch.  On success *dev_ptr is the
+// address kernels use and *is_host (if given) tells whether it is host
+// memory.  With `device_only` pinned host memory is refused too.
+int device_view(const void *ptr, int64_t need, const char *name, void **dev_ptr,
+                bool *is_host = nullptr, bool device_only = false) {
     hipPointerAttribute_t attr;
     hipError_t e = hipPointerGetAttributes(&attr, ptr);
     if (e != hipSuccess) {
@@ -102,6 +105,15 @@ int device_view(const void *ptr, const char *name, void **dev_ptr, bool *is_host
         return fail(KVX_ERR_RANGE, "%s (%p) is not memory the GPU can address (%s)", name, ptr,
                     hipGetErrorString(e));
     }
+    const bool dev_mem = attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged ||
+                         attr.type == hipMemoryTypeUnified;
+    const bool host_mem = attr.type == hipMemoryTypeHost && attr.devicePointer;
+    if (!dev_mem && !host_mem)
+        return fail(KVX_ERR_RANGE, "%s (%p) is not device memory or mapped pinned host memory",
+                    name, ptr);
+    if (device_only && !dev_mem)
+        return fail(KVX_ERR_RANGE, "%s (%p) must be device memory (pinned host memory is refused)",
+                    name, ptr);
     if (attr.type == hipMemoryTypeDevice) {
         // Device memory of another GPU would fault the kernel unless peer
         // access happened to be enabled; this library runs on one GPU.
@@ -113,18 +125,30 @@ int device_view(const void *ptr, const char *name, void **dev_ptr, bool *is_host
             return fail(KVX_ERR_RANGE, "%s (%p) is memory of device %d, but the current device is %d",
                         name, ptr, attr.device, cur);
     }
-    if (attr.type == hipMemoryTypeDevice || attr.type == hipMemoryTypeManaged ||
-        attr.type == hipMemoryTypeUnified) {
-        *dev_ptr = const_cast<void *>(ptr);
-        if (is_host) *is_host = false;
-        return KVX_OK;
+    if (need > 0) {
+        // The allocation around `ptr` must reach `need` bytes past it: a
+        // descriptor larger than its memory would make the kernel read or
+        // write outside the allocation.  Where the runtime reports no
+        // allocation range for the pointer, the extent cannot be checked.
+        hipDeviceptr_t lo = nullptr;
+        size_t size = 0;
+        const hipError_t re = hipMemGetAddressRange(&lo, &size, const_cast<void *>(ptr));
+        if (re != hipSuccess) {
+            (void)hipGetLastError();
+        } else {
+            const uintptr_t a = reinterpret_cast<uintptr_t>(lo), p = reinterpret_cast<uintptr_t>(ptr);
+            const uintptr_t b = a + size;
+            if (p < a || p >= b || (uint64_t)(b - p) < (uint64_t)need)
+                return fail(KVX_ERR_RANGE,
+                            "%s (%p) needs %lld bytes, but its allocation [%p, +%zu) ends %lld "
+                            "bytes after it",
+                            name, ptr, (long long)need, lo, size,
+                            (long long)(p < b && p >= a ? (int64_t)(b - p) : 0));
+        }
     }
-    if (attr.type == hipMemoryTypeHost && attr.devicePointer) {
-        *dev_ptr = attr.devicePointer;
-        if (is_host) *is_host = true;
-        return KVX_OK;
-    }
-    return fail(KVX_ERR_RANGE, "%s (%p) is not device memory or mapped pinned host memory", name, ptr);
+    *dev_ptr = dev_mem ? const_cast<void *>(ptr) : attr.devicePointer;
+    if (is_host) *is_host = !dev_mem;
+    return KVX_OK;
 }
 
 // Byte strides of (layer, page, kv, slot, head) for a pool layout, with the
@@ -201,7 +225,8 @@ int check_buf(const kvx_buf *b, const char *name, Shape &s) {
 
 // Host-only checks of a page table.
 int check_table(const int32_t *pt, int64_t len, const char *name) {
-    if (len < 0) return fail(KVX_ERR_RANGE, "%s: negative length", name);
+    if (len < 0 || len > INT64_MAX / 4) return fail(KVX_ERR_RANGE, "%s: length %lld out of range", name,
+                                                    (long long)len);
     if (len > 0 && !pt) return fail(KVX_ERR_NULL, "%s is NULL but has %lld entries", name, (long long)len);
     if ((reinterpret_cast<uintptr_t>(pt) & 3u) != 0) return fail(KVX_ERR_ALIGN, "%s is not 4-byte aligned", name);
     return KVX_OK;
@@ -227,26 +252,28 @@ struct Views {
     uint32_t *err = nullptr;
 };
 
-int view_all(const void *src, const void *dst, const int32_t *src_pt, int64_t src_pt_len,
-             const int32_t *dst_pt, int64_t dst_pt_len, const kvx_req *reqs, uint32_t *dev_err,
-             Views &v) {
+int view_all(const void *src, int64_t src_bytes, const void *dst, int64_t dst_bytes,
+             const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt, int64_t dst_pt_len,
+             const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err, Views &v) {
     int st;
     void *d = nullptr;
     // A NULL base here is an empty buffer (pools are never NULL): nothing to view.
-    if (src && (st = device_view(src, "src base", &v.src))) return st;
-    if (dst && (st = device_view(dst, "dst base", &v.dst, &v.dst_host))) return st;
+    if (src && (st = device_view(src, src_bytes, "src base", &v.src))) return st;
+    if (dst && (st = device_view(dst, dst_bytes, "dst base", &v.dst, &v.dst_host))) return st;
     if (src_pt_len > 0) {
-        if ((st = device_view(src_pt, "src_pt", &d))) return st;
+        if ((st = device_view(src_pt, src_pt_len * 4, "src_pt", &d))) return st;
         v.src_pt = static_cast<const int32_t *>(d);
     }
     if (dst_pt_len > 0) {
-        if ((st = device_view(dst_pt, "dst_pt", &d))) return st;
+        if ((st = device_view(dst_pt, dst_pt_len * 4, "dst_pt", &d))) return st;
         v.dst_pt = static_cast<const int32_t *>(d);
     }
-    if ((st = device_view(reqs, "reqs", &d))) return st;
+    if ((st = device_view(reqs, (int64_t)n_reqs * (int64_t)sizeof(kvx_req), "reqs", &d))) return st;
     v.reqs = static_cast<const kvx_req *>(d);
     if (dev_err) {
-        if ((st = device_view(dev_err, "dev_err", &d))) return st;
+        // Bits are OR-ed in with device atomics, which pinned host memory
+        // does not support on every platform: the word lives in device memory.
+        if ((st = device_view(dev_err, 4, "dev_err", &d, nullptr, /*device_only=*/true))) return st;
         v.err = static_cast<uint32_t *>(d);
     }
     return KVX_OK;
@@ -336,8 +363,8 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
     }
     const bool empty = n_reqs == 0 || sl.num_layers == 0 || sl.num_kv == 0 || sl.num_heads == 0;
     Views v;
-    if (!empty && (st = view_all(src->base, dst->base, src_pt, src_pt_len, dst_pt, dst_pt_len,
-                                 reqs, dev_err, v)))
+    if (!empty && (st = view_all(src->base, pool_bytes(src), dst->base, pool_bytes(dst), src_pt,
+                                 src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs, dev_err, v)))
         return st;
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     for (int32_t g = 0; g < groups; ++g) {
@@ -423,10 +450,13 @@ int buffer_impl(int op, const kvx_pool *pool, const kvx_buf *buf, const kvx_slic
     if ((st = check_table(pt, pt_len, tname))) return st;
     if (n_reqs == 0) return KVX_OK;
     Views v;
+    const int64_t buf_bytes = buf->capacity_elems * buf->elem_bytes;
     if (gather)
-        st = view_all(pool->base, buf->base, pt, pt_len, nullptr, 0, reqs, dev_err, v);
+        st = view_all(pool->base, pool_bytes(pool), buf->base, buf_bytes, pt, pt_len, nullptr, 0,
+                      reqs, n_reqs, dev_err, v);
     else
-        st = view_all(buf->base, pool->base, nullptr, 0, pt, pt_len, reqs, dev_err, v);
+        st = view_all(buf->base, buf_bytes, pool->base, pool_bytes(pool), nullptr, 0, pt, pt_len,
+                      reqs, n_reqs, dev_err, v);
     if (st) return st;
     const int32_t l0 = gather ? sl.src_layer0 : sl.dst_layer0;
     const int32_t c0 = gather ? sl.src_kv0 : sl.dst_kv0;
@@ -518,8 +548,8 @@ int kvx_page_hashes(const void *payload, int64_t payload_positions, int32_t rec_
         return fail(KVX_ERR_SHAPE, "rec_bytes must be a positive multiple of 4 (got %d)", rec_bytes);
     if (page_tokens < 1 || page_tokens > KVX_MAX_PAGE_TOKENS)
         return fail(KVX_ERR_SHAPE, "page_tokens %d outside [1, %d]", page_tokens, KVX_MAX_PAGE_TOKENS);
-    if (payload_positions < 0 || out_len < 0)
-        return fail(KVX_ERR_RANGE, "payload_positions and out_len must be >= 0");
+    if (payload_positions < 0 || out_len < 0 || out_len > INT64_MAX / 8)
+        return fail(KVX_ERR_RANGE, "payload_positions and out_len must be >= 0 (and out_len < 2^60)");
     if (mul_checked(payload_positions, rec_bytes) < 0)
         return fail(KVX_ERR_RANGE, "payload size exceeds 2^63 bytes");
     if (n_reqs < 0 || n_reqs > KVX_MAX_REQS)
@@ -531,6 +561,8 @@ int kvx_page_hashes(const void *payload, int64_t payload_positions, int32_t rec_
         return fail(KVX_ERR_ALIGN, "payload is not 4-byte aligned");
     if ((reinterpret_cast<uintptr_t>(out) & 7u) != 0 || (reinterpret_cast<uintptr_t>(reqs) & 7u) != 0)
         return fail(KVX_ERR_ALIGN, "out and reqs must be 8-byte aligned");
+    if (!dev_err)
+        return fail(KVX_ERR_NULL, "dev_err is required: it is the only signal of an incomplete chain");
     if ((reinterpret_cast<uintptr_t>(dev_err) & 3u) != 0)
         return fail(KVX_ERR_ALIGN, "dev_err is not 4-byte aligned");
     if (n_reqs == 0) return KVX_OK;
@@ -538,19 +570,18 @@ int kvx_page_hashes(const void *payload, int64_t payload_positions, int32_t rec_
     void *d = nullptr;
     int st;
     if (payload_positions > 0) {
-        if ((st = device_view(payload, "payload", &d))) return st;
+        if ((st = device_view(payload, payload_positions * rec_bytes, "payload", &d))) return st;
         P.payload = static_cast<const uint32_t *>(d);
     }
     if (out_len > 0) {
-        if ((st = device_view(out, "out", &d))) return st;
+        if ((st = device_view(out, out_len * 8, "out", &d))) return st;
         P.out = static_cast<uint64_t *>(d);
     }
-    if ((st = device_view(reqs, "reqs", &d))) return st;
+    if ((st = device_view(reqs, (int64_t)n_reqs * (int64_t)sizeof(kvx_hash_req), "reqs", &d)))
+        return st;
     P.reqs = static_cast<const kvx_hash_req *>(d);
-    if (dev_err) {
-        if ((st = device_view(dev_err, "dev_err", &d))) return st;
-        P.err = static_cast<uint32_t *>(d);
-    }
+    if ((st = device_view(dev_err, 4, "dev_err", &d, nullptr, /*device_only=*/true))) return st;
+    P.err = static_cast<uint32_t *>(d);
     P.payload_positions = payload_positions;
     P.rec_bytes = rec_bytes;
     P.T = page_tokens;

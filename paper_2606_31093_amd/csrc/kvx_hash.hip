@@ -321,14 +321,14 @@ int launch_hash(const HashParams &p0, hipStream_t stream) {
     if (e != hipSuccess) return e;
     HashParams p = p0;
     // Empty polls in a row the chain allows: far more than one page's digest
-    // takes, even with the payload in host memory.  KVX_HASH_IDLE_POLLS
-    // overrides it (tests use a tiny value to see the chain give up cleanly).
+    // takes, even with the payload in host memory.  A build with
+    // KVX_HASH_IDLE_POLLS defined uses that bound instead (a test library
+    // built with a bound of 1 sees the chain give up cleanly).
+#ifdef KVX_HASH_IDLE_POLLS
+    p.idle_limit = (uint64_t)(KVX_HASH_IDLE_POLLS);
+#else
     p.idle_limit = (1ull << 22) + 64ull * (uint64_t)p.T * (uint64_t)p.rec_bytes;
-    if (const char *env = getenv("KVX_HASH_IDLE_POLLS")) {
-        char *end = nullptr;
-        const unsigned long long v = strtoull(env, &end, 10);
-        if (end != env && *end == '\0' && v > 0) p.idle_limit = v;
-    }
+#endif
     // one group per compute unit, each of at most 64 requests
     const int32_t group = (p.n_reqs + cus - 1) / cus;
     p.group = group < 1 ? 1 : group > kSlots ? kSlots : group;

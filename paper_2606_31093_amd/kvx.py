@@ -92,44 +92,49 @@ def lib() -> ctypes.CDLL:
     ``python -m paper_2606_31093_amd.build_lib`` (or ``__graft_entry__.build()``)."""
     global _LIB
     if _LIB is None:
-        path = library_path()
-        if not os.path.exists(path):
-            raise RuntimeError(f"libkvx is not built ({path} missing); run "
-                               "python -m paper_2606_31093_amd.build_lib")
-        # PyTorch ships its own HIP runtime.  Loaded first, it is the one
-        # libkvx binds to (same soname), so the library and torch share one
-        # runtime: the one that owns the tensors and streams passed in.
-        # Loading libkvx first would bring a second HIP and HSA runtime into
-        # the process, and one of them then finds no device.
-        import torch  # noqa: F401
-        L = ctypes.CDLL(path)
-        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
-        pp, bp = ctypes.POINTER(Pool), ctypes.POINTER(Buf)
-        L.kvx_transfer.argtypes = [pp, pp, vp, i64, vp, i64, vp, i32, vp, vp]
-        L.kvx_transfer_slice.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp, i32,
-                                         vp, vp]
-        L.kvx_transfer_layered.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp,
-                                           i32, i32, ctypes.POINTER(vp), i32, vp, vp]
-        L.kvx_gather.argtypes = [pp, bp, vp, i64, vp, i32, vp, vp]
-        L.kvx_scatter.argtypes = [bp, pp, vp, i64, vp, i32, vp, vp]
-        sp = ctypes.POINTER(Slice)
-        L.kvx_gather_slice.argtypes = [pp, bp, sp, vp, i64, vp, i32, vp, vp]
-        L.kvx_scatter_slice.argtypes = [bp, pp, sp, vp, i64, vp, i32, vp, vp]
-        for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_transfer_layered, L.kvx_gather,
-                  L.kvx_scatter, L.kvx_gather_slice, L.kvx_scatter_slice):
-            f.restype = ctypes.c_int
-        L.kvx_page_hashes.argtypes = [vp, i64, i32, i32, vp, i32, vp, i64, vp, vp]
-        L.kvx_page_hashes.restype = ctypes.c_int
-        L.kvx_pool_bytes.argtypes = [pp]
-        L.kvx_pool_bytes.restype = ctypes.c_int64
-        L.kvx_strerror.argtypes = [ctypes.c_int]
-        L.kvx_strerror.restype = ctypes.c_char_p
-        L.kvx_last_error.argtypes = []
-        L.kvx_last_error.restype = ctypes.c_char_p
-        L.kvx_abi_version.argtypes = []
-        L.kvx_abi_version.restype = ctypes.c_int
-        _LIB = L
+        _LIB = load(library_path())
     return _LIB
+
+
+def load(path: str) -> ctypes.CDLL:
+    """Load a build of the library at ``path`` and declare its entry points'
+    argument types (``lib()`` does this once for the default build)."""
+    if not os.path.exists(path):
+        raise RuntimeError(f"libkvx is not built ({path} missing); run "
+                           "python -m paper_2606_31093_amd.build_lib")
+    # PyTorch ships its own HIP runtime.  Loaded first, it is the one
+    # libkvx binds to (same soname), so the library and torch share one
+    # runtime: the one that owns the tensors and streams passed in.
+    # Loading libkvx first would bring a second HIP and HSA runtime into
+    # the process, and one of them then finds no device.
+    import torch  # noqa: F401
+    L = ctypes.CDLL(path)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    pp, bp = ctypes.POINTER(Pool), ctypes.POINTER(Buf)
+    L.kvx_transfer.argtypes = [pp, pp, vp, i64, vp, i64, vp, i32, vp, vp]
+    L.kvx_transfer_slice.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp, i32,
+                                     vp, vp]
+    L.kvx_transfer_layered.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp,
+                                       i32, i32, ctypes.POINTER(vp), i32, vp, vp]
+    L.kvx_gather.argtypes = [pp, bp, vp, i64, vp, i32, vp, vp]
+    L.kvx_scatter.argtypes = [bp, pp, vp, i64, vp, i32, vp, vp]
+    sp = ctypes.POINTER(Slice)
+    L.kvx_gather_slice.argtypes = [pp, bp, sp, vp, i64, vp, i32, vp, vp]
+    L.kvx_scatter_slice.argtypes = [bp, pp, sp, vp, i64, vp, i32, vp, vp]
+    for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_transfer_layered, L.kvx_gather,
+              L.kvx_scatter, L.kvx_gather_slice, L.kvx_scatter_slice):
+        f.restype = ctypes.c_int
+    L.kvx_page_hashes.argtypes = [vp, i64, i32, i32, vp, i32, vp, i64, vp, vp]
+    L.kvx_page_hashes.restype = ctypes.c_int
+    L.kvx_pool_bytes.argtypes = [pp]
+    L.kvx_pool_bytes.restype = ctypes.c_int64
+    L.kvx_strerror.argtypes = [ctypes.c_int]
+    L.kvx_strerror.restype = ctypes.c_char_p
+    L.kvx_last_error.argtypes = []
+    L.kvx_last_error.restype = ctypes.c_char_p
+    L.kvx_abi_version.argtypes = []
+    L.kvx_abi_version.restype = ctypes.c_int
+    return L
 
 
 # ---------------------------------------------------------------------------
@@ -365,11 +370,13 @@ def device_hash_reqs(rows, device="cuda"):
     return torch.from_numpy(pack_hash_reqs(rows).view(np.uint8).copy()).to(device)
 
 
-def kvx_page_hashes(payload, rec_bytes, page_tokens, reqs, out, dev_err=None, stream=None) -> None:
+def kvx_page_hashes(payload, rec_bytes, page_tokens, reqs, out, dev_err, stream=None,
+                    library=None) -> None:
     """Chained page hashes (see kvx_page_hashes in include/kvx.h).  ``payload``
     is a device tensor of records of ``rec_bytes`` bytes, ``reqs`` a device
     tensor from ``device_hash_reqs``, ``out`` a 64-bit device tensor (one
-    word per page)."""
+    word per page) and ``dev_err`` the device error word the call requires.
+    ``library`` is a build loaded with ``load`` (default: ``lib()``)."""
     nbytes = payload.numel() * payload.element_size()
     if nbytes % rec_bytes:
         raise ValueError("payload is not a whole number of records")
@@ -381,9 +388,12 @@ def kvx_page_hashes(payload, rec_bytes, page_tokens, reqs, out, dev_err=None, st
         raise ValueError("reqs must hold whole 32-byte kvx_hash_req records")
     if not reqs.is_contiguous():
         raise ValueError("reqs must be contiguous")
-    _check(lib().kvx_page_hashes(_ptr(payload), nbytes // rec_bytes, int(rec_bytes),
-                                 int(page_tokens), _ptr(reqs), rb // HASH_REQ_DTYPE.itemsize,
-                                 _ptr(out), out.numel(), _ptr(dev_err), _stream(stream)))
+    L = library or lib()
+    status = L.kvx_page_hashes(_ptr(payload), nbytes // rec_bytes, int(rec_bytes),
+                               int(page_tokens), _ptr(reqs), rb // HASH_REQ_DTYPE.itemsize,
+                               _ptr(out), out.numel(), _ptr(dev_err), _stream(stream))
+    if status != 0:
+        raise KvxError(status, L.kvx_last_error().decode())
 
 
 def kvx_strerror(status: int) -> str:

@@ -274,7 +274,17 @@ def test_layered_host_validation(lib):
     ((FAKE, 100, 4, 64, FAKE, 1, FAKE + 4, 10), -3),       # misaligned output
 ])
 def test_page_hash_host_validation(lib, args, status):
-    assert kvx.lib().kvx_page_hashes(*args, None, None) == status
+    assert kvx.lib().kvx_page_hashes(*args, FAKE, None) == status
+
+
+def test_page_hash_requires_error_word(lib):
+    """Without an error word a stalled chain would leave outputs incomplete
+    with no signal, so the call refuses a NULL dev_err, even with nothing to
+    hash."""
+    for n_reqs in (0, 1):
+        assert kvx.lib().kvx_page_hashes(FAKE, 100, 4, 64, FAKE, n_reqs, FAKE, 10, None, None) == -1
+        assert "dev_err" in kvx.kvx_last_error()
+    assert kvx.lib().kvx_page_hashes(FAKE, 100, 4, 64, FAKE, 1, FAKE, 10, FAKE + 2, None) == -3
 
 
 def test_slice_reserved_must_be_zero(lib):
@@ -384,7 +394,8 @@ def test_binding_rejects_wrong_table_and_error_word_types():
         kvx.kvx_transfer(a, P, a, P, t32, t32, strided)
     with pytest.raises(ValueError, match="contiguous"):
         kvx.kvx_page_hashes(torch.zeros(16, dtype=torch.uint8), 4, 4,
-                            torch.zeros(64, dtype=torch.uint8)[::2], torch.zeros(1, dtype=torch.int64))
+                            torch.zeros(64, dtype=torch.uint8)[::2], torch.zeros(1, dtype=torch.int64),
+                            torch.zeros(1, dtype=torch.int32))
 
 
 def test_binding_shares_torchs_hip_runtime():

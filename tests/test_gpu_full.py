@@ -1,10 +1,19 @@
 """Full-size workloads on the GPU, in the launch configuration bench.py
-times, checked against the CPU oracle one layer at a time (layers never mix:
-a layer slice of a pool is a one-layer pool of the same layout)."""
+times, checked against the CPU oracle on every layer (layers never mix: a
+layer slice of a pool is a one-layer pool of the same layout), including the
+bytes the copy must leave untouched.  The per-layer oracle calls run on a
+pool of host threads (ctypes releases the GIL)."""
+import os
+from concurrent.futures import ThreadPoolExecutor
+
 import numpy as np
 import pytest
 
 pytestmark = pytest.mark.gpu
+
+# Host threads for the per-layer checks.  Each holds about three layer
+# slices in host memory (up to 4 GiB for the MLA workload).
+THREADS = max(1, min(8, len(os.sched_getaffinity(0))))
 
 
 @pytest.fixture(scope="module")
@@ -53,6 +62,12 @@ def _run(torch, wl, mem, d):
     return int(err.item())
 
 
+def _each_layer(fn, n_layers):
+    """fn(l) for every layer on the thread pool; returns the results in order."""
+    with ThreadPoolExecutor(THREADS) as ex:
+        return list(ex.map(fn, range(n_layers)))
+
+
 def _free(torch, *objs):
     del objs
     torch.cuda.empty_cache()
@@ -67,65 +82,77 @@ def test_full_transfer(torch, k):
     src = mem[st.src]
     S, D = wl.sides[st.src], wl.sides[st.dst]
     n_layers = st.slice[2] if st.slice is not None else S.L
-    layers = sorted({0, n_layers // 2, n_layers - 1})
     same_pool = st.src == st.dst
-    # a copy inside one pool starts from the pool's values, not a prefill
-    dst_before = {l: layer_check.pool_layer(mem[st.dst], D, l) for l in layers} if same_pool else {}
+    # a copy inside one pool starts from the pool's values, not a prefill: keep
+    # a device copy of the pool as it was
+    pool_before = mem[st.dst].clone() if same_pool else None
     before = int(src.view(torch.int64).sum().item()) if not same_pool else None
-    print(f"{k}: {wl.title}", flush=True)
+    print(f"{k}: {wl.title}; {n_layers} layers on {THREADS} threads", flush=True)
     for _ in range(2):                       # repeated launches write the same bytes
         assert _run(torch, wl, mem, dsteps[0]) == 0
     if not same_pool:
         assert int(src.view(torch.int64).sum().item()) == before, "source pool modified"
-    for l in layers:
+
+    def check(l):
         if st.slice is not None:
             r = layer_check.check_transfer_slice_layer(mem[st.src], S, mem[st.dst], D, st, l,
                                                        wl.prefill_tag)
         else:
+            dst_before = layer_check.pool_layer(pool_before, D, l) if same_pool else None
             r = layer_check.check_transfer_layer(mem[st.src], S, mem[st.dst], D, st, l,
-                                                 wl.prefill_tag, dst_before.get(l))
+                                                 wl.prefill_tag, dst_before)
         print(f"  layer {l}: oracle {r.oracle_seconds:.2f} s, equal={r.equal}", flush=True)
-        assert r.equal, f"{k} layer {l} differs from the oracle"
-    _free(torch, mem, dsteps)
+        return r.equal
+
+    results = _each_layer(check, n_layers)
+    bad = [l for l, ok in enumerate(results) if not ok]
+    assert not bad, f"{k}: layers {bad} differ from the oracle"
+    if st.slice is not None:
+        # layers of the destination outside the slice keep their prefill
+        ld0, nl = st.slice[1], st.slice[2]
+        for l in [x for x in range(D.L) if not ld0 <= x < ld0 + nl]:
+            assert np.array_equal(layer_check.pool_layer(mem[st.dst], D, l),
+                                  layer_check.pool_layer_prefill(D, l, wl.prefill_tag))
+    _free(torch, mem, dsteps, pool_before)
+
+
+def _offload_onload(torch, name, slice_check):
+    from oracle import layer_check
+    wl, mem, dsteps = _setup(torch, name)
+    g, s = wl.steps
+    S, B = wl.sides["A"], wl.sides["buf"]
+    pool_before = mem["A"].clone()
+    assert _run(torch, wl, mem, dsteps[0]) == 0       # offload to pinned host memory
+    assert _run(torch, wl, mem, dsteps[1]) == 0       # onload into fresh pages
+    print(f"{name}: {wl.title}; {S.L} layers on {THREADS} threads", flush=True)
+    per_page = S.nbytes // S.L // S.N
+
+    def check(l):
+        before = layer_check.pool_layer(pool_before, S, l)
+        after = layer_check.pool_layer(mem["A"], S, l)
+        if slice_check:
+            ok_g, ok_s = layer_check.gather_scatter_slice_layer(before, S, mem["buf"], B, after,
+                                                                g, s, l)
+        else:
+            ok_g, ok_s = layer_check.gather_scatter_layer(before, S, mem["buf"], B, after, g, s, l)
+            # round trip: new page k holds the pre-offload bytes of original page k
+            old = before.reshape(S.N, per_page)[g.src_pt]
+            new = after.reshape(S.N, per_page)[s.dst_pt]
+            ok_s = ok_s and np.array_equal(old, new)
+        print(f"  layer {l}: offload equal={ok_g}, onload equal={ok_s}", flush=True)
+        return ok_g and ok_s
+
+    results = _each_layer(check, S.L)
+    bad = [l for l, ok in enumerate(results) if not ok]
+    assert not bad, f"{name}: layers {bad} differ from the oracle"
+    _free(torch, mem, dsteps, pool_before)
 
 
 def test_full_host_offload_onload(torch):
-    from oracle import layer_check
-    wl, mem, dsteps = _setup(torch, "host_tier")
-    g, s = wl.steps
-    S, B = wl.sides["A"], wl.sides["buf"]
-    layers = sorted({0, S.L // 2, S.L - 1})
-    before = {l: layer_check.pool_layer(mem["A"], S, l) for l in layers}
-    assert _run(torch, wl, mem, dsteps[0]) == 0       # offload to pinned host memory
-    assert _run(torch, wl, mem, dsteps[1]) == 0       # onload into fresh pages
-    for l in layers:
-        after = layer_check.pool_layer(mem["A"], S, l)
-        ok_g, ok_s = layer_check.gather_scatter_layer(before[l], S, mem["buf"], B, after, g, s, l)
-        print(f"  layer {l}: offload equal={ok_g}, onload equal={ok_s}", flush=True)
-        assert ok_g and ok_s
-        # round trip: new page k holds the pre-offload bytes of original page k
-        per_page = S.nbytes // S.L // S.N
-        old = before[l].reshape(S.N, per_page)[g.src_pt]
-        new = after.reshape(S.N, per_page)[s.dst_pt]
-        assert np.array_equal(old, new)
-    _free(torch, mem, dsteps)
+    _offload_onload(torch, "host_tier", slice_check=False)
 
 
 def test_full_host_v_only_offload_onload(torch):
     """The host-tier pages, V only: the offload fills a V-only pinned buffer
     and the onload writes only the V half of the fresh pages."""
-    from oracle import layer_check
-    wl, mem, dsteps = _setup(torch, "host_tier_v")
-    g, s = wl.steps
-    S, B = wl.sides["A"], wl.sides["buf"]
-    layers = sorted({0, S.L // 2, S.L - 1})
-    before = {l: layer_check.pool_layer(mem["A"], S, l) for l in layers}
-    assert _run(torch, wl, mem, dsteps[0]) == 0
-    assert _run(torch, wl, mem, dsteps[1]) == 0
-    for l in layers:
-        after = layer_check.pool_layer(mem["A"], S, l)
-        ok_g, ok_s = layer_check.gather_scatter_slice_layer(before[l], S, mem["buf"], B, after,
-                                                            g, s, l)
-        print(f"  layer {l}: V offload equal={ok_g}, V onload equal={ok_s}", flush=True)
-        assert ok_g and ok_s
-    _free(torch, mem, dsteps)
+    _offload_onload(torch, "host_tier_v", slice_check=True)

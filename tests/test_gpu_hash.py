@@ -17,7 +17,7 @@ def torch():
     return torch
 
 
-def _both(torch, payload, rec_bytes, T, rows, out_len, raw=None):
+def _both(torch, payload, rec_bytes, T, rows, out_len, raw=None, library=None):
     from oracle import kvx_oracle
     from paper_2606_31093_amd import kvx
     want = np.full(out_len, 0x5A5A, np.uint64)
@@ -27,7 +27,7 @@ def _both(torch, payload, rec_bytes, T, rows, out_len, raw=None):
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     recs = raw if raw is not None else kvx.pack_hash_reqs(rows)
     reqs = torch.from_numpy(recs.view(np.uint8).copy()).cuda()
-    kvx.kvx_page_hashes(p, rec_bytes, T, reqs, out, err)
+    kvx.kvx_page_hashes(p, rec_bytes, T, reqs, out, err, library=library)
     torch.cuda.synchronize()
     got = out.cpu().numpy().view(np.uint64)
     return got, int(err.item()), want, werr
@@ -223,20 +223,20 @@ def test_pinned_host_payload_and_output(torch, where):
     assert np.array_equal(out.cpu().numpy().view(np.uint64), want)
 
 
-def test_chain_wait_gives_up_cleanly(torch, monkeypatch):
-    """With the chain's wait bound forced down to one empty poll, the chain
-    stops before the first digests exist: the kernel still finishes, raises
-    KVX_DERR_STALLED and leaves the outputs incomplete.  The next call, with
-    the normal bound, is exact again."""
-    from paper_2606_31093_amd import kvx
+def test_chain_wait_gives_up_cleanly(torch):
+    """The test build of the library bounds the chain's wait at one empty
+    poll: the chain stops before the first digests exist, the kernel still
+    finishes, raises KVX_DERR_STALLED and leaves the outputs incomplete.  The
+    next call, through the product library with its normal bound, is exact."""
+    from paper_2606_31093_amd import build_lib, kvx
+    stall = kvx.load(build_lib.STALL_TEST_LIBRARY)
     wl = W.page_hash(small=True)
     pay = W.hash_payload(wl)
-    monkeypatch.setenv("KVX_HASH_IDLE_POLLS", "1")
-    got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
+    got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len,
+                                  library=stall)
     assert werr == 0
     assert gerr & kvx.DERR_STALLED
     assert not np.array_equal(got, want)
-    monkeypatch.delenv("KVX_HASH_IDLE_POLLS")
     got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len)
     assert gerr == werr == 0
     assert np.array_equal(got, want)
