@@ -165,7 +165,7 @@ def main() -> int:
             context["configs"][k] = summary(r)
     out = {
         "metric": METRIC, "value": res["value"], "unit": "GB/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
+        "steps": res["steps"], "warmup": res["warmup"], "ms_per_step": res["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u16",
         "data": "synthetic (seeded N(0,1) bf16 source, offset-coded destination prefill)",
         "config": res["config"],
@@ -180,7 +180,7 @@ def main() -> int:
 def summary(r: dict) -> dict:
     """The per-workload entry of context.configs."""
     c = r["context"]
-    s = {"workload": r["config"]["workload"], "ms_per_step": r["ms_per_step"],
+    s = {"workload": r["config"]["workload"], "steps": r["steps"], "ms_per_step": r["ms_per_step"],
          "value_GBps": r["value"], "roofline": r["roofline"],
          "sample_bit_exact": r["sample_bit_exact"], "sample_layers": r["sample_layers"]}
     for k in ("per_step_kernel_ms", "per_step_kernel_ms_median", "per_step_kernel_ms_min",
@@ -326,7 +326,6 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
 
     # Oracle comparison of sampled layers (and the CPU baseline timing), before
     # the hipMemcpy reference below overwrites the buffers.
-    from oracle import layer_check
     snap = None
     if replay and cpu_layers > 0:
         snap = {side: mem[side].clone() for side in wl.sides if side not in wl.host_sides}
@@ -425,6 +424,7 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
     return {"value": round(value, 1), "ms_per_step": round(ms_per_step, 4), "config": config,
+            "steps": steps, "warmup": warmup,
             "roofline": roofline, "cpu_baseline": cpu, "context": context,
             "sample_bit_exact": exact, "sample_layers": picks}
 

@@ -7,7 +7,7 @@ import ctypes
 import numpy as np
 import pytest
 
-from paper_2606_31093_amd.workloads import BufSpec, PoolSpec, Step, Workload, get
+from paper_2606_31093_amd.workloads import BufSpec, PoolSpec, Step, get
 from runner import assert_same, initial_bytes, run_oracle
 
 pytestmark = pytest.mark.gpu
