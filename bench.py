@@ -107,6 +107,8 @@ def parse():
     ap.add_argument("--cpu-threads", type=int, default=16,
                     help="most host threads for the multi-threaded oracle timing")
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
+    ap.add_argument("--unplanned", action="store_true",
+                    help="launch transfers with kvx_transfer(_slice) instead of kvx_transfer_planned")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (counter calibration)")
     return ap.parse_args()
@@ -194,7 +196,10 @@ def summary(r: dict) -> dict:
 def launch_step(kvx, wl, mem, d, errw):
     st = d["st"]
     S, D = wl.sides[st.src], wl.sides[st.dst]
-    if st.op == "transfer" and st.layer_group:
+    if st.op == "transfer" and d.get("plan") is not None:
+        kvx.kvx_transfer_planned(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
+                                 d["plan"], d["plan_pages"], d["plan_tokens"], st.slice, errw)
+    elif st.op == "transfer" and st.layer_group:
         kvx.kvx_transfer_layered(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
                                  st.layer_group, d["events"], st.slice, errw)
     elif st.op == "transfer" and st.slice is not None:
@@ -240,7 +245,12 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
             reqs=kvx.device_reqs(st.reqs, dev),
             events=[torch.cuda.Event(enable_timing=True)
                     for _ in range(-(-wl.sides[st.src].L // st.layer_group))]
-            if st.layer_group else None))
+            if st.layer_group else None,
+            # the plan of destination pages, built on the host from the records
+            # and uploaded with them (kvx_transfer_planned)
+            **(dict(zip(("plan", "plan_pages", "plan_tokens"),
+                        kvx.device_plan(st.reqs, wl.sides[st.src].T, wl.sides[st.dst].T, dev)))
+               if st.op == "transfer" and not st.layer_group and not args.unplanned else {})))
     errw = torch.zeros(1, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 
@@ -414,7 +424,9 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
 
     n_tok = sum(st.n_tokens for st in wl.steps)
     config = {"workload": wl.title, "name": name,
-              "ops": [st.op for st in wl.steps], "requests": len(wl.steps[0].reqs),
+              "ops": [("transfer_planned" if d.get("plan") is not None else st.op)
+                      for st, d in zip(wl.steps, dsteps)],
+              "requests": len(wl.steps[0].reqs),
               "tokens_per_step": n_tok, "bytes_per_step": step_bytes,
               "pools": {k: {"bytes": v.nbytes, **({"layout": v.layout, "page_tokens": v.T}
                                                   if hasattr(v, "layout") else {})}

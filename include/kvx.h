@@ -60,6 +60,8 @@
  *   - KVX_DERR_PT_RANGE: a table index outside [0, pt_len);
  *   - KVX_DERR_BAD_REQ: a malformed request record.  The whole record is
  *     skipped.
+ *   - KVX_DERR_BAD_PLAN (kvx_transfer_planned only): the plan disagrees
+ *     with the records;
  *   - KVX_DERR_STALLED (kvx_page_hashes only): the chain of a group waited
  *     longer than its bound for a digest and gave up; outputs of that group
  *     are incomplete.  The bound is far beyond any digest time, so this
@@ -122,6 +124,7 @@ typedef enum kvx_status {
 #define KVX_DERR_PT_RANGE 4u
 #define KVX_DERR_BAD_REQ 8u
 #define KVX_DERR_STALLED 16u
+#define KVX_DERR_BAD_PLAN 32u
 
 /* A paged pool of num_pages pages; element (l, p, c, t, h, d) lives where
  * `layout` puts it.  `base` is device memory (or device-mapped pinned host
@@ -269,6 +272,84 @@ int kvx_scatter_slice(const kvx_buf *src, const kvx_pool *dst, const kvx_slice *
                       const int32_t *dst_pt, int64_t dst_pt_len,
                       const kvx_req *reqs, int32_t n_reqs,
                       uint32_t *dev_err, void *stream);
+
+/* One destination page of a planned transfer (32 bytes): where request
+ * `req` writes its page jj, that is, the tokens [dst_slot, dst_slot +
+ * n_tokens) of destination page dst_pt[dst_idx], read from the source page
+ * src_pt[src_idx] from slot src_slot on (and on into the following source
+ * pages).  Indices outside the int32 range are stored clamped to it. */
+typedef struct kvx_plan_slot {
+    int32_t dst_idx;    /* index in dst_pt of the page */
+    int32_t src_idx;    /* index in src_pt of the page holding the first token */
+    int32_t dst_slot;   /* first slot written in the page */
+    int32_t n_tokens;   /* tokens written in the page, >= 1 */
+    int32_t src_slot;   /* slot of the first token in its source page */
+    int32_t req;        /* the record */
+    int32_t reserved[2];
+} kvx_plan_slot;
+
+/* Bytes of a plan of n_reqs records and plan_pages destination pages. */
+#define KVX_PLAN_BYTES(n_reqs, plan_pages) (((int64_t)(n_reqs) + 1) * 8 + (int64_t)(plan_pages) * 32)
+
+/* kvx_transfer / kvx_transfer_slice (slice NULL: everything) with a plan,
+ * for callers that build their records on the host.  The plan spells out,
+ * page by page, the work the records imply, so that the kernel copying a
+ * piece of a page finds it with one read instead of a search:
+ * plan: device memory (or mapped pinned host memory), KVX_PLAN_BYTES bytes,
+ *   8-byte aligned, written by kvx_plan_fill():
+ *   - int64 prefix[n_reqs + 1]: the exclusive prefix over the records of
+ *     the destination pages each touches, pages(r) = (dst_start + n_tokens
+ *     - 1) / T_dst - dst_start / T_dst + 1 for a well-formed record with
+ *     n_tokens > 0, else 0 (a malformed record, as in the kvx_req rules,
+ *     counts 0);
+ *   - kvx_plan_slot slots[plan_pages], in record order, page order within
+ *     a record.
+ * plan_pages: prefix[n_reqs]; plan_tokens: n_tokens summed over the
+ *   well-formed records (kvx_plan_pages returns both).  Read on the host to
+ *   shape the launch.
+ * When the destination is token-major (LPCTHD or PLCTHD, every head), the
+ * records copy at least 96 KiB per destination page and layer on average,
+ * and both tables hold at most INT32_MAX entries, the library launches one
+ * workgroup per 1 KiB piece of each destination page of each layer, layer
+ * by layer and page by page, instead of a persistent grid.  Started in that
+ * order by the hardware, the pieces in flight stay within a small window
+ * that slides through the transfer; on MI355X this holds the handoff's 256
+ * KiB pages at 5.7-5.9 TB/s in every process, where the persistent grid
+ * ranges from 5.1 to 6.3 TB/s with the physical placement of the pools.
+ * Otherwise the call runs as the unplanned one and the plan is not read.
+ * Results, error bits and every rule are those of kvx_transfer(_slice):
+ * - a plan that disagrees with the records, or with the pools' page sizes,
+ *   raises KVX_DERR_BAD_PLAN, and the destination is then defined only
+ *   where the plan and the records agree (every access still stays inside
+ *   the pools and tables); plan_pages other than prefix[n_reqs] is such a
+ *   disagreement;
+ * - a wrong plan_tokens changes only the choice of launch.
+ * plan_pages or plan_tokens < 0, a NULL plan with n_reqs > 0, or a plan
+ * extent below KVX_PLAN_BYTES is refused on the host. */
+int kvx_transfer_planned(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                         const int32_t *src_pt, int64_t src_pt_len,
+                         const int32_t *dst_pt, int64_t dst_pt_len,
+                         const kvx_req *reqs, int32_t n_reqs,
+                         const void *plan, int64_t plan_pages, int64_t plan_tokens,
+                         uint32_t *dev_err, void *stream);
+
+/* Sizes a plan from a host copy of the records: writes the exclusive prefix
+ * of pages per record into prefix[0..n_reqs] and the tokens of the
+ * well-formed records into *tokens (each if not NULL), and returns the
+ * total of pages, for the side `side` (0: source positions, 1: destination
+ * positions) of a pool with page_tokens tokens per page.  -1 on bad
+ * arguments. */
+int64_t kvx_plan_pages(const kvx_req *host_reqs, int32_t n_reqs, int32_t page_tokens, int32_t side,
+                       int64_t *prefix, int64_t *tokens);
+
+/* Writes the plan of kvx_transfer_planned for these records and page sizes
+ * into host memory `plan` of KVX_PLAN_BYTES(n_reqs, plan_pages) bytes,
+ * 8-byte aligned; plan_pages must be the total kvx_plan_pages returns for
+ * side 1 and dst_page_tokens.  KVX_ERR_RANGE on bad arguments or a
+ * plan_pages that differs from that total, KVX_ERR_NULL / KVX_ERR_ALIGN for
+ * the pointers. */
+int kvx_plan_fill(const kvx_req *host_reqs, int32_t n_reqs, int32_t src_page_tokens,
+                  int32_t dst_page_tokens, int64_t plan_pages, void *plan);
 
 /* One chained-hash request (32 bytes). */
 typedef struct kvx_hash_req {

@@ -15,10 +15,13 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libkvx.so")
-# A test build whose hash chain gives up after one empty poll (the bound is a
-# compile-time option, so the product library has no switch for it).
-STALL_TEST_LIBRARY = os.path.join(PKG, "libkvx_test_stall.so")
-STALL_TEST_DEFINES = ("KVX_HASH_IDLE_POLLS=1",)
+# The test build: its hash chain gives up after one empty poll, and planned
+# transfers of any size and destination layout take the sweep launch, with
+# at most 2048 workgroups, so that larger cases loop over page slots.  These are compile-time
+# options: the product library has no switch for them.
+TEST_LIBRARY = os.path.join(PKG, "libkvx_test.so")
+TEST_DEFINES = ("KVX_HASH_IDLE_POLLS=1", "KVX_SWEEP_MIN_BYTES=0", "KVX_SWEEP_MAX_BLOCKS=2048",
+                "KVX_SWEEP_HEAD_MAJOR=1")
 SOURCES = [os.path.join(CSRC, "kvx_kernels.hip"), os.path.join(CSRC, "kvx_hash.hip"),
            os.path.join(CSRC, "kvx_api.cpp")]
 HEADERS = [os.path.join(INCLUDE, "kvx.h"), os.path.join(CSRC, "kvx_internal.h"),
@@ -61,7 +64,7 @@ def is_stale(output: str = LIBRARY) -> bool:
 
 def build_all() -> list:
     """The library and its test build."""
-    return [build(), build(STALL_TEST_LIBRARY, STALL_TEST_DEFINES)]
+    return [build(), build(TEST_LIBRARY, TEST_DEFINES)]
 
 
 if __name__ == "__main__":

@@ -296,6 +296,7 @@ void finish_params(kvx::Params &P, const Shape &s, const Views &v, int32_t n_req
     P.fd_vpr = kvx::make_fastdiv((uint32_t)P.vpr);
     P.fd_H = kvx::make_fastdiv((uint32_t)P.H);
     P.fd_To = kvx::make_fastdiv((uint32_t)os.T);
+    P.fd_Tt = kvx::make_fastdiv((uint32_t)(P.op == kvx::OP_GATHER ? P.src : P.dst).T);
 }
 
 int enqueue(const kvx::Params &P, void *stream) {
@@ -331,11 +332,50 @@ int check_slice(const kvx_slice &sl, const Shape &s, const Shape &d) {
 // Pool -> pool; slice == NULL copies everything between equal shapes.  With
 // group > 0 the layer range is moved in groups of `group` layers, one launch
 // each, and events[g] is recorded on the stream after group g.
+// A planned transfer whose shape the sweep kernel serves well gets its
+// launch: a token-major destination (measured: a head-major one splits each
+// piece into row-sized fragments and runs slower than the persistent grid),
+// at least KVX_SWEEP_MIN_BYTES copied per destination page and layer on
+// average, page tables whose indices fit in int32, and a grid of at most
+// KVX_SWEEP_MAX_BLOCKS workgroups per pass.  Otherwise, and for unplanned
+// calls, the persistent grid.  The test build sweeps head-major
+// destinations too, to keep that path covered.
+void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t plan_tokens) {
+    P.sweep = 0;
+    if (!plan || plan_pages < 1 || plan_tokens < 1 || P.n_reqs < 1 || P.op != kvx::OP_TRANSFER) return;
+    if (P.src.pt_len > INT32_MAX || P.dst.pt_len > INT32_MAX) return;
+    if (!P.dst.tok_contig && !KVX_SWEEP_HEAD_MAJOR) return;
+    const int64_t T = P.dst.T, rows_per_head =
+        P.dst.tok_contig ? T : (T + KVX_SLOT_BLOCK - 1) / KVX_SLOT_BLOCK * KVX_SLOT_BLOCK + KVX_SLOT_BLOCK;
+    // average bytes copied per destination page and layer
+    const int64_t token_bytes = (int64_t)P.C * P.H * P.row_bytes;
+    if (plan_tokens > INT64_MAX / token_bytes || plan_tokens * token_bytes < KVX_SWEEP_MIN_BYTES * plan_pages)
+        return;
+    // pieces of 64 vectors per page: the vectors of the page's enumeration (a
+    // head-major destination covers whole slot blocks, a few slots more)
+    const int64_t tile_vecs = (int64_t)P.C * rows_per_head * P.H * P.vpr;
+    const int64_t ppt = (tile_vecs + 63) / 64;
+    const int64_t per_slot = (int64_t)P.L * ppt;         // workgroups per page slot
+    if (per_slot > KVX_SWEEP_MAX_BLOCKS) return;
+    const int64_t slots = plan_pages < KVX_SWEEP_MAX_BLOCKS / per_slot ? plan_pages
+                                                                      : KVX_SWEEP_MAX_BLOCKS / per_slot;
+    P.sweep = 1;
+    P.prefix = static_cast<const int64_t *>(plan);
+    P.slots = reinterpret_cast<const kvx_plan_slot *>(P.prefix + P.n_reqs + 1);
+    P.plan_pages = plan_pages;
+    P.sweep_pages = (int32_t)slots;
+    P.sweep_ppt = (uint32_t)ppt;
+    P.fd_ppt = kvx::make_fastdiv((uint32_t)ppt);
+    P.fd_sp = kvx::make_fastdiv((uint32_t)slots);
+    P.fd_hv = kvx::make_fastdiv((uint32_t)(P.H * P.vpr));
+}
+
 int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
                   const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
                   int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err,
                   void *stream, int32_t group = 0, void *const *events = nullptr,
-                  int32_t n_events = 0) {
+                  int32_t n_events = 0, const void *plan = nullptr, int64_t plan_pages = -1,
+                  int64_t plan_tokens = -1) {
     Shape ss, ds;
     int st;
     if ((st = check_pool(src, "src", ss))) return st;
@@ -366,6 +406,11 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
     if (!empty && (st = view_all(src->base, pool_bytes(src), dst->base, pool_bytes(dst), src_pt,
                                  src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs, dev_err, v)))
         return st;
+    if (!empty && plan) {
+        void *d = nullptr;
+        if ((st = device_view(plan, KVX_PLAN_BYTES(n_reqs, plan_pages), "plan", &d))) return st;
+        plan = d;
+    }
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     for (int32_t g = 0; g < groups; ++g) {
         if (!empty) {
@@ -378,6 +423,7 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
             P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, sl.dst_layer0 + l0, sl.dst_kv0,
                               sl.dst_head0, sl.num_heads);
             finish_params(P, Shape{nl, sl.num_kv, sl.num_heads, ss.D, ss.e}, v, n_reqs);
+            if (group == 0) plan_sweep(P, plan, plan_pages, plan_tokens);
             if ((st = enqueue(P, stream))) return st;
         }
         if (group > 0) {
@@ -526,6 +572,81 @@ int kvx_scatter_slice(const kvx_buf *src, const kvx_pool *dst, const kvx_slice *
     if (!slice) return fail(KVX_ERR_NULL, "slice is NULL");
     return buffer_impl(kvx::OP_SCATTER, dst, src, slice, dst_pt, dst_pt_len, reqs, n_reqs, dev_err,
                        stream);
+}
+
+int kvx_transfer_planned(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                         const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
+                         int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs, const void *plan,
+                         int64_t plan_pages, int64_t plan_tokens, uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    // the prefix holds n_reqs + 1 words and every record has fewer than 2^31 pages
+    if (plan_pages < 0 || plan_tokens < 0 || plan_pages > (int64_t)KVX_MAX_REQS * INT32_MAX)
+        return fail(KVX_ERR_RANGE, "plan_pages and plan_tokens must be >= 0 (got %lld, %lld)",
+                    (long long)plan_pages, (long long)plan_tokens);
+    if (n_reqs > 0 && !plan) return fail(KVX_ERR_NULL, "plan is NULL");
+    if ((reinterpret_cast<uintptr_t>(plan) & 7u) != 0) return fail(KVX_ERR_ALIGN, "plan is not 8-byte aligned");
+    return transfer_impl(src, dst, slice, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
+                         dev_err, stream, 0, nullptr, 0, plan, plan_pages, plan_tokens);
+}
+
+int64_t kvx_plan_pages(const kvx_req *host_reqs, int32_t n_reqs, int32_t page_tokens, int32_t side,
+                       int64_t *prefix, int64_t *tokens) {
+    g_last_error.clear();
+    if (n_reqs < 0 || n_reqs > KVX_MAX_REQS || (n_reqs > 0 && !host_reqs) || page_tokens < 1 ||
+        (side != 0 && side != 1)) {
+        fail(KVX_ERR_RANGE, "kvx_plan_pages: bad arguments");
+        return -1;
+    }
+    int64_t pages = 0, n_tok = 0;
+    for (int32_t r = 0; r < n_reqs; ++r) {
+        if (prefix) prefix[r] = pages;
+        const kvx_req &R = host_reqs[r];
+        // a malformed record (the kvx_req rules that do not depend on a buffer) counts 0
+        const int64_t s0 = R.src_start, d0 = R.dst_start, n = R.n_tokens;
+        if (n <= 0 || s0 < 0 || d0 < 0 || R.reserved != 0 || s0 + n > INT32_MAX || d0 + n > INT32_MAX)
+            continue;
+        const int64_t start = side ? d0 : s0;
+        pages += (start + n - 1) / page_tokens - start / page_tokens + 1;
+        n_tok += n;
+    }
+    if (prefix) prefix[n_reqs] = pages;
+    if (tokens) *tokens = n_tok;
+    return pages;
+}
+
+namespace {
+int32_t clamp_i32(int64_t x) { return x < INT32_MIN ? INT32_MIN : x > INT32_MAX ? INT32_MAX : (int32_t)x; }
+}  // namespace
+
+int kvx_plan_fill(const kvx_req *host_reqs, int32_t n_reqs, int32_t src_page_tokens,
+                  int32_t dst_page_tokens, int64_t plan_pages, void *plan) {
+    g_last_error.clear();
+    if (n_reqs < 0 || n_reqs > KVX_MAX_REQS || src_page_tokens < 1 || dst_page_tokens < 1 || plan_pages < 0)
+        return fail(KVX_ERR_RANGE, "kvx_plan_fill: bad arguments");
+    if ((n_reqs > 0 && !host_reqs) || !plan) return fail(KVX_ERR_NULL, "kvx_plan_fill: NULL pointer");
+    if ((reinterpret_cast<uintptr_t>(plan) & 7u) != 0) return fail(KVX_ERR_ALIGN, "plan is not 8-byte aligned");
+    int64_t *prefix = static_cast<int64_t *>(plan);
+    const int64_t total = kvx_plan_pages(host_reqs, n_reqs, dst_page_tokens, 1, prefix, nullptr);
+    if (total != plan_pages)
+        return fail(KVX_ERR_RANGE, "plan_pages %lld differs from the records' %lld pages",
+                    (long long)plan_pages, (long long)total);
+    kvx_plan_slot *slot = reinterpret_cast<kvx_plan_slot *>(prefix + n_reqs + 1);
+    const int64_t Td = dst_page_tokens, Ts = src_page_tokens;
+    for (int32_t r = 0; r < n_reqs; ++r) {
+        const kvx_req &R = host_reqs[r];
+        const int64_t pages = prefix[r + 1] - prefix[r];
+        const int64_t d0 = R.dst_start, s0 = R.src_start, end = d0 + R.n_tokens;
+        for (int64_t jj = 0; jj < pages; ++jj, ++slot) {
+            const int64_t j = d0 / Td + jj, page_lo = j * Td;
+            const int64_t qa = page_lo > d0 ? page_lo : d0;
+            const int64_t qb = page_lo + Td < end ? page_lo + Td : end;
+            const int64_t pos = qa - d0 + s0;              // source position of the first token
+            *slot = kvx_plan_slot{clamp_i32(R.dst_pt_off + j), clamp_i32(R.src_pt_off + pos / Ts),
+                                  (int32_t)(qa - page_lo), (int32_t)(qb - qa), (int32_t)(pos % Ts), r,
+                                  {0, 0}};
+        }
+    }
+    return KVX_OK;
 }
 
 int kvx_transfer_layered(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,

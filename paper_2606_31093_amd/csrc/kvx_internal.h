@@ -7,6 +7,26 @@
 
 #include "kvx.h"
 
+#ifndef KVX_SLOT_BLOCK
+#define KVX_SLOT_BLOCK 2  // head-major tiling: slots per block of the vector order (measured best)
+#endif
+// A planned transfer sweeps when its records copy at least this many bytes
+// per destination page and layer on average (measured).
+#ifndef KVX_SWEEP_MIN_BYTES
+#define KVX_SWEEP_MIN_BYTES (96 << 10)
+#endif
+// Whether planned transfers into a head-major destination sweep (the test
+// build only).
+#ifndef KVX_SWEEP_HEAD_MAJOR
+#define KVX_SWEEP_HEAD_MAJOR 0
+#endif
+// Most workgroups of one sweep launch: the work-items of a launch (64 per
+// workgroup) must stay below 2^32, and this keeps them below 2^31.  Beyond
+// it, workgroups loop over page slots.
+#ifndef KVX_SWEEP_MAX_BLOCKS
+#define KVX_SWEEP_MAX_BLOCKS (INT32_MAX / 64)
+#endif
+
 namespace kvx {
 
 // Unsigned division by a divisor fixed for a launch, for dividends below
@@ -16,24 +36,22 @@ namespace kvx {
 // n / 2^31 < 1 / d of one quotient step (Granlund and Montgomery,
 // "Division by invariant integers using multiplication", PLDI 1994).
 struct FastDiv {
-    uint32_t d;  // divisor, 1 <= d < 2^31
-    uint32_t m;  // multiplier (unused when d == 1)
-    uint32_t s;  // post-shift l - 1
+    uint32_t d;   // divisor, 1 <= d < 2^31
+    uint32_t m;   // ceil(2^(31 + l) / d), l = ceil(log2 d); below 2^32
+    uint32_t sh;  // 31 + l
 };
 
 inline FastDiv make_fastdiv(uint32_t d) {
-    FastDiv f{d, 0u, 0u};
-    if (d > 1) {
-        uint32_t l = 0;
-        while ((1ull << l) < d) ++l;
-        f.m = (uint32_t)(((1ull << (31 + l)) + d - 1) / d);
-        f.s = l - 1;
-    }
-    return f;
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    return FastDiv{d, (uint32_t)(((1ull << (31 + l)) + d - 1) / d), 31 + l};
 }
 
+// n / d for n < 2^31 without a branch: n * m / 2^(31 + l) = n / d + n * (m *
+// d - 2^(31 + l)) / (d * 2^(31 + l)), and the second term, below n / 2^(31 +
+// l) < 2^-l <= 1 / d, cannot reach the next multiple of 1 / d.
 __host__ __device__ inline uint32_t fd_div(const FastDiv &f, uint32_t n) {
-    return f.d == 1 ? n : (uint32_t)(((uint64_t)n * f.m) >> 32) >> f.s;
+    return (uint32_t)(((uint64_t)n * f.m) >> f.sh);
 }
 
 // One side of a copy.  A pool side addresses row (l, page, c, slot, h) at
@@ -68,6 +86,21 @@ struct Params {
     int32_t flat;        // both sides tok_contig: a tile is C contiguous runs per piece
     int32_t dst_host;    // the destination is pinned host memory (plain stores)
     FastDiv fd_vpr, fd_H, fd_To;
+    FastDiv fd_Tt;       // tiling side's page_tokens
+    // Sweep launch (a planned pool -> pool transfer): one workgroup per piece
+    // of 64 vectors of one destination page of one layer.  sweep_pages page
+    // slots per layer are launched (at most plan_pages; workgroups go on to
+    // the slots sweep_pages apart when the launch is capped), sweep_ppt
+    // pieces per page.  prefix[r] = destination pages of records 0..r-1,
+    // slots[q] = page q of the plan.  sweep == 0: persistent grid.
+    int32_t sweep;
+    int32_t sweep_pages;
+    uint32_t sweep_ppt;
+    int64_t plan_pages;
+    FastDiv fd_ppt, fd_sp;
+    FastDiv fd_hv;       // H * vpr: vectors per token of a token-major side
+    const int64_t *prefix;
+    const kvx_plan_slot *slots;
 };
 
 // Launch on `stream`; returns a hipError_t value.

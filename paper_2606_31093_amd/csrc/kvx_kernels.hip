@@ -55,9 +55,6 @@
 #ifndef KVX_BLOCK
 #define KVX_BLOCK 256
 #endif
-#ifndef KVX_SLOT_BLOCK
-#define KVX_SLOT_BLOCK 2  // head-major tiling: slots per block of the vector order (measured best)
-#endif
 #ifndef KVX_FLAT_WAVE_TILES
 #define KVX_FLAT_WAVE_TILES 1  // launches of contiguous runs: one tile per wavefront
 #endif
@@ -107,6 +104,7 @@ struct Req {
     int64_t t_pt_off, o_pt_off;  // table offsets of the tiling / other side
     int64_t blk;                 // buffer block offset in bytes
     int64_t tiles;               // tiles this request contributes
+    int64_t pages;               // tiling-side pages it touches (tiles = pages * layers)
     int32_t t_start, o_start, n;
     int32_t j0;                  // first tiling-side page (logical)
 };
@@ -130,6 +128,7 @@ __device__ __forceinline__ bool load_req(const Params &p, int32_t r, Req &q) {
     if (OP == OP_SCATTER) ok = ok && s0 == 0 && block_fits(p.src, bo, n, token_bytes, p.elem_bytes);
     if (!ok) {
         q.tiles = 0;
+        q.pages = 0;
         return false;
     }
     const bool tsrc = OP == OP_GATHER;
@@ -142,22 +141,25 @@ __device__ __forceinline__ bool load_req(const Params &p, int32_t r, Req &q) {
     const Side &ts = tsrc ? p.src : p.dst;
     if (n == 0) {
         q.tiles = 0;
+        q.pages = 0;
         q.j0 = 0;
         return true;
     }
-    const int32_t j0 = q.t_start / ts.T;
-    const int32_t j1 = (q.t_start + n - 1) / ts.T;
+    const int32_t j0 = (int32_t)fd_div(p.fd_Tt, (uint32_t)q.t_start);
+    const int32_t j1 = (int32_t)fd_div(p.fd_Tt, (uint32_t)(q.t_start + n - 1));
     q.j0 = j0;
-    q.tiles = (int64_t)(j1 - j0 + 1) * p.L;
+    q.pages = j1 - j0 + 1;
+    q.tiles = q.pages * p.L;
     return true;
 }
 
-// Plain vector stream over C runs of R vectors each, by a worker of NT threads.
+// Plain vector stream over C runs of R vectors each, by a worker of NT threads:
+// the vectors [kb, ke) of the tile in (c, vector) order.
 template <int NT, int U, bool HOST>
 __device__ __forceinline__ void copy_runs(char *d, const char *s, int64_t d_sc, int64_t s_sc,
-                                          uint32_t R, int32_t C) {
-    const uint32_t total = R * (uint32_t)C;
-    for (uint32_t k0 = worker_tid<NT>(); k0 < total; k0 += NT * U) {
+                                          uint32_t R, int32_t C, uint32_t kb, uint32_t ke) {
+    const uint32_t total = R * (uint32_t)C < ke ? R * (uint32_t)C : ke;
+    for (uint32_t k0 = kb + worker_tid<NT>(); k0 < total; k0 += NT * U) {
         v4u v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -200,7 +202,8 @@ struct Tile {
 // blocks of slots as described below, with the slots outside [sa, sb)
 // masked.
 template <int OP, bool TTHD, int NT, bool HOST, int U>
-__device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const Tile &t) {
+__device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const Tile &t, uint32_t kb0,
+                                          uint32_t ke) {
     constexpr bool kTileSrc = OP == OP_GATHER;
     constexpr bool kOtherBuf = OP != OP_TRANSFER;
     const Side &ts = kTileSrc ? p.src : p.dst;
@@ -215,11 +218,11 @@ __device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const T
     constexpr uint32_t SB = KVX_SLOT_BLOCK;
     const uint32_t blk0 = (uint32_t)t.sa / SB, nblk = ((uint32_t)t.sb - 1) / SB - blk0 + 1;
     const uint32_t rows_c = TTHD ? (uint32_t)t.ntok * H : H * nblk * SB;
-    const uint32_t total = rows_c * vpr * (uint32_t)p.C;
+    const uint32_t total = rows_c * vpr * (uint32_t)p.C < ke ? rows_c * vpr * (uint32_t)p.C : ke;
     const char *o_l = os.base + (int64_t)t.l * os.s_l;
     // The trip count is the same for every lane: the page-id broadcast below
     // reads other lanes, which must all still be active.
-    for (uint32_t kb = 0; kb < total; kb += NT * U) {
+    for (uint32_t kb = kb0; kb < total; kb += NT * U) {
         const char *src[U];
         char *dst[U];
         bool ok[U];
@@ -286,16 +289,18 @@ __device__ __forceinline__ void copy_rows(const Params &p, const Req &q, const T
     }
 }
 
-template <int OP, bool TTHD, int NT, bool HOST>
-__device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t local) {
+// Tile (request q, its tiling-side page jj, layer l): the vectors [kb, ke) of
+// the tile's vector order, U vectors per thread in flight.
+template <int OP, bool TTHD, int NT, bool HOST, int UF, int UR>
+__device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t jj, int32_t layer,
+                                        uint32_t kb, uint32_t ke) {
     constexpr bool kTileSrc = OP == OP_GATHER;
     constexpr bool kOtherBuf = OP != OP_TRANSFER;
     const Side &ts = kTileSrc ? p.src : p.dst;
     const Side &os = kTileSrc ? p.dst : p.src;
 
     Tile t;
-    const int64_t jj = local / p.L;
-    t.l = (int32_t)(local - jj * p.L);
+    t.l = layer;
     const int64_t j = q.j0 + jj;
     const int64_t page_lo = j * ts.T;
     const int64_t qa = page_lo > q.t_start ? page_lo : q.t_start;
@@ -330,18 +335,18 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
         if (p.flat) {
             const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
             if (kTileSrc)
-                copy_runs<NT, KVX_UNROLL_FLAT, HOST>(const_cast<char *>(t.o_row0), tb, t.o_sc, ts.s_c,
-                                           (uint32_t)run_t, p.C);
+                copy_runs<NT, UF, HOST>(const_cast<char *>(t.o_row0), tb, t.o_sc, ts.s_c,
+                                        (uint32_t)run_t, p.C, kb, ke);
             else
-                copy_runs<NT, KVX_UNROLL_FLAT, HOST>(const_cast<char *>(tb), t.o_row0, ts.s_c, t.o_sc,
-                                           (uint32_t)run_t, p.C);
+                copy_runs<NT, UF, HOST>(const_cast<char *>(tb), t.o_row0, ts.s_c, t.o_sc,
+                                        (uint32_t)run_t, p.C, kb, ke);
             return;
         }
     } else {
         const int32_t delta = q.o_start - q.t_start;
         t.qo_a = (int32_t)qa + delta;
-        t.jo0 = t.qo_a / os.T;
-        const int32_t jo1 = ((int32_t)qb - 1 + delta) / os.T;
+        t.jo0 = (int32_t)fd_div(p.fd_To, (uint32_t)t.qo_a);
+        const int32_t jo1 = (int32_t)fd_div(p.fd_To, (uint32_t)((int32_t)qb - 1 + delta));
         const int32_t K = jo1 - t.jo0 + 1;
         const int32_t lane = threadIdx.x & (kWave - 1);
         t.pid = -1;
@@ -364,12 +369,12 @@ __device__ __forceinline__ void do_tile(const Params &p, const Req &q, int64_t l
             const char *ob = os.base + (int64_t)t.l * os.s_l + (int64_t)pg * os.s_p +
                              (int64_t)so0 * os.s_t;
             const char *tb = t.t_base + (int64_t)t.sa * ts.s_t;
-            copy_runs<NT, KVX_UNROLL_FLAT, HOST>(const_cast<char *>(tb), ob, ts.s_c, os.s_c,
-                                       (uint32_t)run_t, p.C);
+            copy_runs<NT, UF, HOST>(const_cast<char *>(tb), ob, ts.s_c, os.s_c, (uint32_t)run_t,
+                                    p.C, kb, ke);
             return;
         }
     }
-    copy_rows<OP, TTHD, NT, HOST, KVX_UNROLL_ROWS>(p, q, t);
+    copy_rows<OP, TTHD, NT, HOST, UR>(p, q, t, kb, ke);
 }
 
 // Inclusive sum of x over the workgroup's threads (x = 0 past the chunk).
@@ -423,10 +428,218 @@ __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
                 load_req<OP>(p, r0 + lo, q);
                 cached = r0 + lo;
             }
-            do_tile<OP, TTHD, NT, HOST>(p, q, local - (lo ? s_end[lo - 1] : 0));
+            const int64_t in_rec = local - (lo ? s_end[lo - 1] : 0);
+            const int64_t jj = in_rec / p.L;
+            do_tile<OP, TTHD, NT, HOST, KVX_UNROLL_FLAT, KVX_UNROLL_ROWS>(
+                p, q, jj, (int32_t)(in_rec - jj * p.L), 0u, 0xFFFFFFFFu);
         }
         chunk_base += chunk_tiles;
         __syncthreads();                             // s_end and s_wave are rewritten next chunk
+    }
+}
+
+// Lane k's row of a tile in the vector order of copy_rows: kv component c,
+// slot, head h, vector v of the row; valid is cleared for a masked slot of a
+// head-major tiling side.
+template <bool TTHD>
+__device__ __forceinline__ void tile_row(const Params &p, uint32_t k, uint32_t rows_c, int32_t sa,
+                                         int32_t sb, uint32_t blk0, uint32_t &c, uint32_t &slot,
+                                         uint32_t &h, uint32_t &v, bool &valid) {
+    constexpr uint32_t SB = KVX_SLOT_BLOCK;
+    const uint32_t rw = fd_div(p.fd_vpr, k);
+    v = k - rw * p.vpr;
+    c = rw >= rows_c;
+    const uint32_t rr = rw - c * rows_c;
+    if (TTHD) {
+        const uint32_t tt = fd_div(p.fd_H, rr);
+        h = rr - tt * p.H;
+        slot = (uint32_t)sa + tt;
+    } else {
+        const uint32_t q1 = rr / SB;
+        const uint32_t blk = fd_div(p.fd_H, q1);
+        h = q1 - blk * p.H;
+        slot = (blk0 + blk) * SB + (rr - q1 * SB);
+        valid = valid && slot >= (uint32_t)sa && slot < (uint32_t)sb;
+    }
+}
+
+// One piece of the sweep: the vectors [kb, kb + 64) of destination page slot
+// d of layer l, one vector per lane, in the vector order of copy_rows (a
+// head-major destination in blocks of slots, the slots outside the page's
+// range masked).  Every load of metadata on the path that copies (the slot,
+// the destination page id, and the source page id when all the piece's rows
+// lie in one source page, the usual case) is uniform and comes before the
+// first store or atomic, so it goes through the scalar cache.  FLAT (both
+// sides token-major with every head): the page is C runs of contiguous
+// vectors on both sides, the piece's source pages are found from its first
+// and last vectors, and a piece in one source page is a plain vector copy.
+// Errors are reported for the positions the piece covers, destination
+// first.  The slot's fields are only trusted as far as keeping every access
+// inside the pools and tables; whether they match the records is checked
+// separately (check_slot).
+template <bool TTHD, bool FLAT, bool HOST>
+__device__ __forceinline__ void sweep_piece(const Params &p, const kvx_plan_slot &d, uint32_t l,
+                                            uint32_t kb) {
+    const Side &ts = p.dst, &os = p.src;
+    const int32_t sa = d.dst_slot, so_a = d.src_slot;
+    const uint32_t ntok = (uint32_t)d.n_tokens;
+    if (!((uint32_t)sa < (uint32_t)ts.T && ntok - 1u < (uint32_t)(ts.T - sa) &&
+          (uint32_t)so_a < (uint32_t)os.T))
+        return;
+    const int32_t sb = sa + (int32_t)ntok;
+    constexpr uint32_t SB = KVX_SLOT_BLOCK;
+    const uint32_t blk0 = (uint32_t)sa / SB, nblk = ((uint32_t)sb - 1) / SB - blk0 + 1;
+    const uint32_t rows_c = TTHD ? ntok * p.H : p.H * nblk * SB;
+    const uint32_t total = rows_c * p.vpr * (uint32_t)p.C;
+    if (kb >= total) return;
+    const uint32_t lane = threadIdx.x;
+    const uint32_t k = kb + lane;
+    bool valid = k < total;
+
+    // per lane: the row (FLAT: kv component and vector of the run) and its
+    // source page, counted from the slot's; jo0 is that of the first live lane
+    uint32_t c = 0, slot = 0, h = 0, v = 0, jo, jo0, w = 0;
+    if (FLAT) {
+        const uint32_t R = ntok * p.H * p.vpr;                 // vectors per kv run
+        const uint32_t kc = valid ? k : kb;
+        c = kc >= R;
+        w = kc - c * R;
+        jo = fd_div(p.fd_To, (uint32_t)so_a + fd_div(p.fd_hv, w));
+        jo0 = __builtin_amdgcn_readfirstlane(jo);              // lane 0 is live
+    } else {
+        tile_row<TTHD>(p, valid ? k : total - 1, rows_c, sa, sb, blk0, c, slot, h, v, valid);
+        const uint64_t live = __ballot(valid);
+        if (live == 0) return;
+        jo = fd_div(p.fd_To, (uint32_t)so_a + (slot - (uint32_t)sa));
+        jo0 = __builtin_amdgcn_readlane(jo, __builtin_ctzll(live));
+    }
+    const bool one = __ballot(valid && jo != jo0) == 0;
+    // The sweep runs only on tables of at most INT32_MAX entries, so 32-bit
+    // unsigned compares also reject negative indices (jo0 < 2^21 cannot
+    // carry a non-negative src_idx past 2^32).
+    const bool t_in = (uint32_t)d.dst_idx < (uint32_t)ts.pt_len;
+    const uint32_t oidx0 = (uint32_t)d.src_idx + jo0;
+    const bool o_in = d.src_idx >= 0 && oidx0 < (uint32_t)os.pt_len;
+    // both page ids are read before any error is reported (an atomic ahead
+    // of them would turn them into vector loads)
+    const int32_t tpage = t_in ? ts.pt[(uint32_t)d.dst_idx] : -1;
+    const int32_t opage0 = t_in && one && o_in ? os.pt[oidx0] : -1;
+    const bool pages_ok = (uint32_t)tpage < (uint32_t)ts.N && (uint32_t)opage0 < (uint32_t)os.N;
+    char *t_base = ts.base + (int64_t)l * ts.s_l + (int64_t)tpage * ts.s_p;
+    const char *o_l = os.base + (int64_t)l * os.s_l;
+    if (FLAT && one && pages_ok) {
+        // the usual case: the piece's rows in one source page, both pages valid
+        if (!valid) return;
+        // source slot of the page's first token, counted from source page jo0
+        const int64_t so = (int64_t)so_a - (int64_t)jo0 * os.T;
+        const char *s = o_l + (int64_t)opage0 * os.s_p + so * os.s_t;
+        char *dd = t_base + (int64_t)sa * ts.s_t;
+        st16<HOST>(dd + c * ts.s_c + (int64_t)w * 16, ld16(s + c * os.s_c + (int64_t)w * 16));
+        return;
+    }
+    // errors of the page and of a single source page, destination first
+    if (!t_in || (uint32_t)tpage >= (uint32_t)ts.N) {
+        if (lane == 0) report(p, t_in ? KVX_DERR_DST_PAGE : KVX_DERR_PT_RANGE);
+        return;
+    }
+    if (one && !pages_ok) {
+        if (lane == 0) report(p, o_in ? KVX_DERR_SRC_PAGE : KVX_DERR_PT_RANGE);
+        return;
+    }
+    if (FLAT) {                     // rows in two source pages: resolve them as the general case
+        tile_row<true>(p, valid ? k : total - 1, rows_c, sa, sb, blk0, c, slot, h, v, valid);
+        jo = fd_div(p.fd_To, (uint32_t)so_a + (slot - (uint32_t)sa));
+    }
+    int32_t pg = one ? opage0 : -1;
+    if (!one && valid) {
+        const int64_t idx = (int64_t)d.src_idx + jo;
+        if (idx < 0 || idx >= os.pt_len) {
+            report(p, KVX_DERR_PT_RANGE);
+        } else {
+            const int32_t id = os.pt[idx];
+            if (id < 0 || id >= os.N) report(p, KVX_DERR_SRC_PAGE);
+            else pg = id;
+        }
+    }
+    if (!valid || pg < 0) return;
+    const uint32_t so = (uint32_t)so_a + (slot - (uint32_t)sa) - jo * (uint32_t)os.T;
+    const char *src = o_l + (int64_t)pg * os.s_p + c * os.s_c + (int64_t)so * os.s_t +
+                      (int64_t)h * os.s_h + v * 16;
+    char *dst = t_base + c * ts.s_c + (int64_t)slot * ts.s_t + (int64_t)h * ts.s_h + v * 16;
+    st16<HOST>(dst, ld16(src));
+}
+
+__device__ __forceinline__ int32_t clamp_i32(int64_t x) {
+    return x < INT32_MIN ? INT32_MIN : x > INT32_MAX ? INT32_MAX : (int32_t)x;
+}
+
+// Whether slot d of the plan is page qi of the plan the records imply: its
+// record's prefix range holds qi, and its fields are those of that record's
+// page qi - prefix[r].  Run once per slot (by one workgroup of layer 0).
+__device__ __forceinline__ bool slot_agrees(const Params &p, int64_t qi, const kvx_plan_slot &d) {
+    const int32_t r = d.req;
+    if (r < 0 || r >= p.n_reqs) return false;
+    Req q;
+    if (!load_req<OP_TRANSFER>(p, r, q)) return false;
+    const int64_t jj = qi - p.prefix[r];
+    if (jj < 0 || qi >= p.prefix[r + 1] || jj >= q.pages) return false;
+    const int64_t j = (int64_t)q.j0 + jj, page_lo = j * p.dst.T;
+    const int64_t q_end = (int64_t)q.t_start + q.n;
+    const int64_t qa = page_lo > q.t_start ? page_lo : q.t_start;
+    const int64_t qb = page_lo + p.dst.T < q_end ? page_lo + p.dst.T : q_end;
+    const int64_t pos = qa - q.t_start + q.o_start;
+    const int64_t jo = pos / p.src.T;
+    return d.dst_idx == clamp_i32(q.t_pt_off + j) && d.src_idx == clamp_i32(q.o_pt_off + jo) &&
+           d.dst_slot == (int32_t)(qa - page_lo) && d.n_tokens == (int32_t)(qb - qa) &&
+           d.src_slot == (int32_t)(pos - jo * p.src.T);
+}
+
+// Page slot qi of layer l: read its slot, copy the piece, and (one workgroup
+// per slot) check the slot against the records.
+template <bool TTHD, bool FLAT, bool HOST>
+__device__ __forceinline__ void sweep_slot(const Params &p, int64_t qi, uint32_t l, uint32_t piece) {
+    const kvx_plan_slot d = p.slots[qi];
+    sweep_piece<TTHD, FLAT, HOST>(p, d, l, piece * kWave);
+    if (l == 0 && piece == 0 && !slot_agrees(p, qi, d) && threadIdx.x == 0) report(p, KVX_DERR_BAD_PLAN);
+}
+
+// Sweep kernel (a planned pool -> pool transfer): one wavefront per
+// workgroup, and workgroup b copies one piece of 64 vectors (1 KiB) of one
+// destination page of one layer, found by one read of the plan.  Workgroups
+// are numbered layer by layer, page by page within a layer (pages in plan
+// order), piece by piece within a page, so the hardware dispatcher, which
+// starts them in order, keeps the pieces in flight on the whole GPU inside a
+// small window that slides through the transfer.  (A persistent grid lets
+// its workers drift over the whole transfer; on the same pools this order
+// moves 10-20% more bytes per second for 256 KiB pages.)  The launch has
+// layers x sweep_pages x ppt workgroups; when sweep_pages is below
+// plan_pages (a capped launch), workgroups go on to the slots sweep_pages
+// apart.  The first slot is taken outside that loop, so that its loads
+// precede every store of the kernel.  Workgroup 0 finally checks the
+// prefix against the records and plan_pages, and reports malformed records.
+template <bool TTHD, bool FLAT, bool HOST>
+__global__ void __launch_bounds__(kWave) kvx_sweep_kernel(Params p) {
+    const uint32_t b = blockIdx.x;
+    const uint32_t slot = fd_div(p.fd_ppt, b);                 // (layer, page slot)
+    const uint32_t piece = b - slot * p.sweep_ppt;
+    const uint32_t l = fd_div(p.fd_sp, slot);
+    const int64_t q0 = (int64_t)(slot - l * (uint32_t)p.sweep_pages);
+    sweep_slot<TTHD, FLAT, HOST>(p, q0, l, piece);
+    for (int64_t qi = q0 + p.sweep_pages; qi < p.plan_pages; qi += p.sweep_pages)  // capped launch
+        sweep_slot<TTHD, FLAT, HOST>(p, qi, l, piece);
+    if (b == 0) {
+        // prefix[0] = 0, prefix[r + 1] - prefix[r] = pages of record r, and
+        // prefix[n_reqs] = plan_pages
+        bool bad_plan = p.prefix[0] != 0 || p.prefix[p.n_reqs] != p.plan_pages;
+        for (int32_t r0 = 0; r0 < p.n_reqs; r0 += kWave) {
+            const int32_t r = r0 + (int32_t)threadIdx.x;
+            if (r < p.n_reqs) {
+                Req mine;
+                if (!load_req<OP_TRANSFER>(p, r, mine)) report(p, KVX_DERR_BAD_REQ);
+                bad_plan = bad_plan || p.prefix[r + 1] - p.prefix[r] != mine.pages;
+            }
+        }
+        if (bad_plan) report(p, KVX_DERR_BAD_PLAN);
     }
 }
 
@@ -456,8 +669,21 @@ KernelFn pick(int op, bool tthd, bool flat, bool host) {
 
 }  // namespace
 
-// Persistent grid: as many workgroups as the device holds at once.
+// Sweep grid when the host chose it (p.sweep), else a persistent grid: as
+// many workgroups as the device holds at once.
 int launch(const Params &p, hipStream_t stream) {
+    if (p.sweep) {
+        KernelFn fs;
+        if (p.flat)
+            fs = p.dst_host ? kvx_sweep_kernel<true, true, true> : kvx_sweep_kernel<true, true, false>;
+        else if (p.dst.tok_contig)
+            fs = p.dst_host ? kvx_sweep_kernel<true, false, true> : kvx_sweep_kernel<true, false, false>;
+        else
+            fs = p.dst_host ? kvx_sweep_kernel<false, false, true> : kvx_sweep_kernel<false, false, false>;
+        const uint64_t blocks = (uint64_t)p.L * (uint64_t)p.sweep_pages * p.sweep_ppt;
+        hipLaunchKernelGGL(fs, dim3((uint32_t)blocks), dim3(kWave), 0, stream, p);
+        return hipGetLastError();
+    }
     const bool tthd = (p.op == OP_GATHER ? p.src : p.dst).tok_contig != 0;
     KernelFn fn = pick(p.op, tthd, p.flat != 0, p.dst_host != 0);
     int dev = 0;

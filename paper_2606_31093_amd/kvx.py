@@ -4,7 +4,7 @@ Every step of the copy runs in the library's HIP kernels.  PyTorch supplies
 device memory and the stream: tensors are passed as raw pointers and the
 kernels run on ``torch.cuda.current_stream()`` unless a stream is given.
 The functions keep the C names: ``kvx_transfer``, ``kvx_transfer_slice``,
-``kvx_transfer_layered``, ``kvx_gather``, ``kvx_scatter``,
+``kvx_transfer_layered``, ``kvx_transfer_planned``, ``kvx_gather``, ``kvx_scatter``,
 ``kvx_gather_slice``, ``kvx_scatter_slice`` and ``kvx_page_hashes``.  A missing or unloadable library raises; there is no
 fallback path.
 
@@ -29,6 +29,7 @@ DERR_DST_PAGE = 2
 DERR_PT_RANGE = 4
 DERR_BAD_REQ = 8
 DERR_STALLED = 16
+DERR_BAD_PLAN = 32
 
 STATUS = {0: "KVX_OK", -1: "KVX_ERR_NULL", -2: "KVX_ERR_SHAPE", -3: "KVX_ERR_ALIGN",
           -4: "KVX_ERR_LAYOUT", -5: "KVX_ERR_RANGE", -6: "KVX_ERR_HIP"}
@@ -124,6 +125,13 @@ def load(path: str) -> ctypes.CDLL:
     for f in (L.kvx_transfer, L.kvx_transfer_slice, L.kvx_transfer_layered, L.kvx_gather,
               L.kvx_scatter, L.kvx_gather_slice, L.kvx_scatter_slice):
         f.restype = ctypes.c_int
+    L.kvx_transfer_planned.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp, i32,
+                                       vp, i64, i64, vp, vp]
+    L.kvx_transfer_planned.restype = ctypes.c_int
+    L.kvx_plan_pages.argtypes = [vp, i32, i32, i32, vp, vp]
+    L.kvx_plan_pages.restype = ctypes.c_int64
+    L.kvx_plan_fill.argtypes = [vp, i32, i32, i32, i64, vp]
+    L.kvx_plan_fill.restype = ctypes.c_int
     L.kvx_page_hashes.argtypes = [vp, i64, i32, i32, vp, i32, vp, i64, vp, vp]
     L.kvx_page_hashes.restype = ctypes.c_int
     L.kvx_pool_bytes.argtypes = [pp]
@@ -172,6 +180,14 @@ def pack_reqs(rows) -> np.ndarray:
             raise ValueError(f"{name} does not fit int32")
         out[name] = col
     return out
+
+
+def _records(rows) -> np.ndarray:
+    """kvx_req records: ``rows`` itself if it already is a record array,
+    else pack_reqs(rows)."""
+    if isinstance(rows, np.ndarray) and rows.dtype == REQ_DTYPE:
+        return rows
+    return pack_reqs(rows)
 
 
 def device_reqs(rows, device="cuda"):
@@ -279,6 +295,81 @@ def kvx_transfer_slice(src, src_spec, dst, dst_spec, sl, src_pt, dst_pt, reqs, d
     _check(lib().kvx_transfer_slice(ctypes.byref(S), ctypes.byref(D), ctypes.byref(X),
                                     _ptr(src_pt), _len(src_pt), _ptr(dst_pt), _len(dst_pt),
                                     _ptr(reqs), _n_reqs(reqs), _ptr(dev_err), _stream(stream)))
+
+
+def kvx_transfer_planned(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, plan, plan_pages,
+                         plan_tokens, sl=None, dev_err=None, stream=None, library=None) -> None:
+    """Pool -> pool with a plan (see kvx_transfer_planned in
+    include/kvx.h): ``plan`` a device tensor holding the plan, and
+    ``plan_pages``, ``plan_tokens`` its totals, as ``device_plan`` returns.  ``sl`` is an optional
+    slice (nine range fields or a ``Slice``); ``library`` a build loaded with
+    ``load`` (default: ``lib()``)."""
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    S, D = pool_desc(src_spec, src), pool_desc(dst_spec, dst)
+    X = ctypes.byref(slice_desc(sl)) if sl is not None else None
+    _table(src_pt, "src_pt"), _table(dst_pt, "dst_pt"), _err_word(dev_err)
+    n = _n_reqs(reqs)
+    if plan is not None and not isinstance(plan, int):
+        if not plan.is_contiguous() or plan.numel() * plan.element_size() < plan_bytes(n, plan_pages):
+            raise ValueError("plan must be a contiguous tensor of KVX_PLAN_BYTES(n_reqs, plan_pages) "
+                             "bytes")
+    L = library or lib()
+    status = L.kvx_transfer_planned(ctypes.byref(S), ctypes.byref(D), X, _ptr(src_pt), _len(src_pt),
+                                    _ptr(dst_pt), _len(dst_pt), _ptr(reqs), n, _ptr(plan),
+                                    int(plan_pages), int(plan_tokens), _ptr(dev_err),
+                                    _stream(stream))
+    if status != 0:
+        raise KvxError(status, L.kvx_last_error().decode())
+
+
+def plan_pages(rows, page_tokens: int, side: int = 1):
+    """kvx_plan_pages on a host copy of the (n, 6) rows: the exclusive prefix
+    of pages per record (numpy int64, n + 1 entries), the total of pages and
+    the tokens of the well-formed records, for side 0 (source) or 1
+    (destination) of a pool with ``page_tokens`` tokens per page.  ``rows``
+    may also be a kvx_req record array."""
+    recs = _records(rows)
+    prefix = np.zeros(len(recs) + 1, np.int64)
+    tokens = ctypes.c_int64(0)
+    n = int(lib().kvx_plan_pages(recs.ctypes.data if len(recs) else None, len(recs), int(page_tokens),
+                                 int(side), prefix.ctypes.data, ctypes.byref(tokens)))
+    if n < 0:
+        raise KvxError(-5, lib().kvx_last_error().decode())
+    return prefix, n, tokens.value
+
+
+def plan_bytes(n_reqs: int, plan_pages: int) -> int:
+    """KVX_PLAN_BYTES: the prefix (n_reqs + 1 int64) and the 32-byte slots."""
+    return (int(n_reqs) + 1) * 8 + int(plan_pages) * 32
+
+
+def host_plan(rows, src_page_tokens: int, dst_page_tokens: int):
+    """kvx_plan_fill for the (n, 6) rows (or a kvx_req record array): the
+    plan as a host int64 array (the prefix, then four words per slot), its
+    pages and its tokens."""
+    recs = _records(rows)
+    _, pages, tokens = plan_pages(recs, dst_page_tokens, 1)
+    buf = np.zeros(plan_bytes(len(recs), pages) // 8, np.int64)
+    st = lib().kvx_plan_fill(recs.ctypes.data if len(recs) else None, len(recs), int(src_page_tokens),
+                             int(dst_page_tokens), pages, buf.ctypes.data)
+    if st != 0:
+        raise KvxError(st, lib().kvx_last_error().decode())
+    return buf, pages, tokens
+
+
+def plan_slots(buf, n_reqs: int):
+    """The slots of a host plan as an (pages, 8) int32 array (a view):
+    dst_idx, src_idx, dst_slot, n_tokens, src_slot, req and two reserved."""
+    return buf[n_reqs + 1:].view(np.int32).reshape(-1, 8)
+
+
+def device_plan(rows, src_page_tokens: int, dst_page_tokens: int, device="cuda"):
+    """The plan of ``rows`` on the device: (tensor, pages, tokens), the
+    arguments of kvx_transfer_planned after the records."""
+    import torch
+    buf, pages, tokens = host_plan(rows, src_page_tokens, dst_page_tokens)
+    return torch.from_numpy(buf).to(device), pages, tokens
 
 
 def kvx_transfer_layered(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, layers_per_group,

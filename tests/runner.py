@@ -47,9 +47,13 @@ def run_oracle(wl, init: dict, reqs_override=None) -> tuple[dict, list]:
     return mem, errs
 
 
-def run_gpu(wl, init: dict, raw_reqs=None) -> tuple[dict, list]:
+def run_gpu(wl, init: dict, raw_reqs=None, planned=None, library=None) -> tuple[dict, list]:
     """Apply every step with libkvx on cuda:0.  ``raw_reqs`` may give kvx_req
-    record arrays (numpy structured) per step instead of the (n, 6) rows."""
+    record arrays (numpy structured) per step instead of the (n, 6) rows.
+    With ``planned``, transfer steps go through kvx_transfer_planned, in
+    ``library`` (a build from kvx.load; default the product library), with
+    their plan: ``planned`` takes the host plan (int64 array), its pages and
+    tokens and returns the three to pass (the same, or altered)."""
     import torch
 
     from paper_2606_31093_amd import kvx
@@ -74,7 +78,14 @@ def run_gpu(wl, init: dict, raw_reqs=None) -> tuple[dict, list]:
         S, D = wl.sides[st.src], wl.sides[st.dst]
         spt = kvx.device_table(st.src_pt, dev) if st.src_pt is not None else None
         dpt = kvx.device_table(st.dst_pt, dev) if st.dst_pt is not None else None
-        if st.op == "transfer" and st.layer_group:
+        if st.op == "transfer" and planned is not None and not st.layer_group:
+            buf, pages, tokens = kvx.host_plan(raw_reqs[i] if raw_reqs is not None else st.reqs,
+                                               S.T, D.T)
+            buf, pages, tokens = planned(buf, pages, tokens)
+            kvx.kvx_transfer_planned(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs,
+                                     torch.from_numpy(buf).to(dev), pages, tokens, st.slice, err,
+                                     library=library)
+        elif st.op == "transfer" and st.layer_group:
             n_layers = st.slice[2] if st.slice is not None else S.L
             events = [torch.cuda.Event() for _ in range(-(-n_layers // st.layer_group))]
             kvx.kvx_transfer_layered(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs,

@@ -433,3 +433,126 @@ def test_empty_buffer_may_have_no_memory(lib):
     full = kvx.buf_desc(BufSpec(GOOD.L, GOOD.C, GOOD.H, GOOD.D, GOOD.e, cap=1 << 10), 0)
     assert L.kvx_gather(ctypes.byref(pd), ctypes.byref(full), FAKE, 1, FAKE, 0, None, None) == -1
     assert "base is NULL" in kvx.kvx_last_error()
+
+
+def _pages_reference(rows, T, side):
+    """Pages a record touches on one side: the positions [start, start + n)
+    of the record, page q // T for each position q, counted once."""
+    total = 0
+    for so, do, bo, s0, d0, n in rows:
+        start = d0 if side else s0
+        if n <= 0 or start < 0:
+            continue
+        total += len({q // T for q in range(start, start + n)})
+    return total
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_plan_pages_matches_a_position_count(lib, seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(0, 40))
+    rows = [[0, 0, 0, int(rng.integers(0, 300)), int(rng.integers(0, 300)), int(rng.integers(-2, 200))]
+            for _ in range(n)]
+    for T in (1, 3, 16, 64):
+        for side in (0, 1):
+            prefix, total, tokens = kvx.plan_pages(rows, T, side)
+            per = [_pages_reference([r], T, side) for r in rows]
+            assert total == sum(per)
+            assert tokens == sum(max(r[5], 0) for r in rows)
+            assert prefix.tolist() == [0] + np.cumsum(per, dtype=np.int64).tolist()
+
+
+def test_plan_pages_counts_malformed_records_as_empty(lib):
+    recs = kvx.pack_reqs([[0, 0, 0, 0, 0, 5], [0, 0, 0, 2**31 - 3, 0, 5], [0, 0, 0, 0, 0, 5]])
+    recs["reserved"][2] = 1
+    prefix = np.full(4, -7, np.int64)
+    tokens = ctypes.c_int64(-7)
+    assert lib.kvx_plan_pages(recs.ctypes.data, 3, 4, 0, prefix.ctypes.data, ctypes.byref(tokens)) == 2
+    assert prefix.tolist() == [0, 2, 2, 2] and tokens.value == 5
+
+
+def test_plan_pages_bad_arguments(lib):
+    recs = kvx.pack_reqs([[0, 0, 0, 0, 0, 5]])
+    c = lib.kvx_plan_pages
+    assert c(recs.ctypes.data, 1, 0, 1, None, None) == -1          # no page size
+    assert c(recs.ctypes.data, 1, 16, 2, None, None) == -1         # side not 0 or 1
+    assert c(None, 1, 16, 1, None, None) == -1                     # records missing
+    assert c(None, 0, 16, 1, None, None) == 0
+    assert c(recs.ctypes.data, -1, 16, 1, None, None) == -1
+    assert c(recs.ctypes.data, 1, 16, 1, None, None) == 1          # outputs optional
+
+
+def _plan_reference(rows, Ts, Td):
+    """The slots of a plan from the definition: for each destination page a
+    record touches, in record order, the page's table index, the tokens it
+    receives, and the table index and slot of the source position of its
+    first token."""
+    out = []
+    for r, (so, do, _bo, s0, d0, n) in enumerate(rows):
+        if n <= 0 or s0 < 0 or d0 < 0 or s0 + n >= 2**31 or d0 + n >= 2**31:
+            continue
+        for j in range(d0 // Td, (d0 + n - 1) // Td + 1):
+            first, last = max(j * Td, d0), min((j + 1) * Td, d0 + n)
+            pos = first - d0 + s0
+            out.append([do + j, so + pos // Ts, first - j * Td, last - first, pos % Ts, r, 0, 0])
+    return np.asarray(out, np.int64).reshape(-1, 8)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_plan_fill_matches_the_definition(lib, seed):
+    rng = np.random.default_rng(100 + seed)
+    n = int(rng.integers(1, 30))
+    rows = [[int(rng.integers(0, 50)), int(rng.integers(0, 50)), 0, int(rng.integers(0, 300)),
+             int(rng.integers(0, 300)), int(rng.integers(-2, 150))] for _ in range(n)]
+    for Ts, Td in ((1, 1), (3, 16), (16, 3), (64, 64), (7, 5)):
+        buf, pages, tokens = kvx.host_plan(rows, Ts, Td)
+        prefix, total, _ = kvx.plan_pages(rows, Td, 1)
+        assert pages == total and buf.size * 8 == kvx.plan_bytes(n, pages)
+        assert buf[:n + 1].tolist() == prefix.tolist()
+        assert kvx.plan_slots(buf, n).tolist() == _plan_reference(rows, Ts, Td).tolist()
+
+
+def test_plan_fill_clamps_table_indices(lib):
+    rows = [[2**40, -2**40, 0, 0, 3, 3]]
+    buf, pages, _ = kvx.host_plan(rows, 4, 4)
+    assert pages == 2
+    assert kvx.plan_slots(buf, 1)[:, :2].tolist() == [[-2**31, 2**31 - 1], [-2**31, 2**31 - 1]]
+
+
+def test_plan_fill_bad_arguments(lib):
+    recs = kvx.pack_reqs([[0, 0, 0, 0, 0, 5]])
+    buf = np.zeros(kvx.plan_bytes(1, 1) // 8 + 1, np.int64)
+    f = lib.kvx_plan_fill
+    assert f(recs.ctypes.data, 1, 4, 8, 1, buf.ctypes.data) == 0
+    assert f(recs.ctypes.data, 1, 4, 8, 2, buf.ctypes.data) == -5       # not the records' total
+    assert f(recs.ctypes.data, 1, 0, 8, 1, buf.ctypes.data) == -5       # no page size
+    assert f(recs.ctypes.data, -1, 4, 8, 1, buf.ctypes.data) == -5
+    assert f(None, 1, 4, 8, 1, buf.ctypes.data) == -1
+    assert f(recs.ctypes.data, 1, 4, 8, 1, None) == -1
+    assert f(recs.ctypes.data, 1, 4, 8, 1, buf.ctypes.data + 4) == -3
+    assert f(None, 0, 4, 8, 0, buf.ctypes.data) == 0
+
+
+def test_planned_transfer_host_validation(lib):
+    """The planned transfer checks its plan arguments and otherwise applies
+    the plain transfer's host checks."""
+    S = PoolSpec(1, 2, 1, 8, T=4, N=4, e=2, layout="LPCTHD")
+    P = ctypes.byref(kvx.pool_desc(S, FAKE))
+    call = lib.kvx_transfer_planned
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, FAKE, -1, 4, None, None) == -5
+    assert "plan_pages" in kvx.kvx_last_error()
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, FAKE, 1, -4, None, None) == -5
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, None, 3, 4, None, None) == -1
+    assert "plan" in kvx.kvx_last_error()
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, FAKE + 4, 3, 4, None, None) == -3
+    assert call(None, P, None, FAKE, 4, FAKE, 4, FAKE, 1, FAKE, 3, 4, None, None) == -1
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, -1, FAKE, 3, 4, None, None) == -5
+    bad = ctypes.byref(kvx.pool_desc(PoolSpec(1, 2, 1, 7, T=4, N=4, e=2), FAKE))
+    assert call(bad, bad, None, FAKE, 4, FAKE, 4, FAKE, 1, FAKE, 3, 4, None, None) == -3
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 0, None, 0, 0, None, None) == 0   # nothing to do
+
+
+def test_test_build_exports_the_same_functions():
+    out = subprocess.run(["nm", "-D", "--defined-only", build_lib.TEST_LIBRARY], capture_output=True,
+                         text=True, check=True).stdout
+    assert set(declared_functions()) <= set(re.findall(r"\b(kvx_\w+)$", out, flags=re.M))

@@ -40,12 +40,19 @@ def _setup(torch, k):
     return wl, mem, dsteps
 
 
-def _run(torch, wl, mem, d):
+def _run(torch, wl, mem, d, planned=True):
+    """One step as bench.py launches it: a transfer goes through
+    kvx_transfer_planned with the plan of its destination pages
+    (planned=False: the plain call)."""
     from paper_2606_31093_amd import kvx
     st = d["st"]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     S, D = wl.sides[st.src], wl.sides[st.dst]
-    if st.op == "transfer" and st.slice is not None:
+    if st.op == "transfer" and planned:
+        plan, pages, tokens = kvx.device_plan(st.reqs, S.T, D.T)
+        kvx.kvx_transfer_planned(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
+                                 plan, pages, tokens, st.slice, err)
+    elif st.op == "transfer" and st.slice is not None:
         kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, d["spt"], d["dpt"],
                                d["reqs"], err)
     elif st.op == "transfer":
@@ -73,9 +80,10 @@ def _free(torch, *objs):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("k", ["handoff", "relayout", "mla", "tp_reshard", "cow_fork",
-                               "small_requests"])
-def test_full_transfer(torch, k):
+@pytest.mark.parametrize("k,planned", [("handoff", True), ("handoff", False), ("relayout", True),
+                                     ("mla", True), ("tp_reshard", True), ("cow_fork", True),
+                                     ("small_requests", True)])
+def test_full_transfer(torch, k, planned):
     from oracle import layer_check
     wl, mem, dsteps = _setup(torch, k)
     st = dsteps[0]["st"]
@@ -89,7 +97,7 @@ def test_full_transfer(torch, k):
     before = int(src.view(torch.int64).sum().item()) if not same_pool else None
     print(f"{k}: {wl.title}; {n_layers} layers on {THREADS} threads", flush=True)
     for _ in range(2):                       # repeated launches write the same bytes
-        assert _run(torch, wl, mem, dsteps[0]) == 0
+        assert _run(torch, wl, mem, dsteps[0], planned) == 0
     if not same_pool:
         assert int(src.view(torch.int64).sum().item()) == before, "source pool modified"
 

@@ -229,7 +229,7 @@ def test_chain_wait_gives_up_cleanly(torch):
     finishes, raises KVX_DERR_STALLED and leaves the outputs incomplete.  The
     next call, through the product library with its normal bound, is exact."""
     from paper_2606_31093_amd import build_lib, kvx
-    stall = kvx.load(build_lib.STALL_TEST_LIBRARY)
+    stall = kvx.load(build_lib.TEST_LIBRARY)
     wl = W.page_hash(small=True)
     pay = W.hash_payload(wl)
     got, gerr, want, werr = _both(torch, pay, wl.rec_bytes, wl.T, wl.rows, wl.out_len,
