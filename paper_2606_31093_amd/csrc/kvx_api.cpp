@@ -354,7 +354,8 @@ void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t pl
     // pieces of 64 vectors per page: the vectors of the page's enumeration (a
     // head-major destination covers whole slot blocks, a few slots more)
     const int64_t tile_vecs = (int64_t)P.C * rows_per_head * P.H * P.vpr;
-    const int64_t ppt = (tile_vecs + 63) / 64;
+    // workgroups per page: KVX_SWEEP_PIECES pieces each
+    const int64_t ppt = ((tile_vecs + 63) / 64 + KVX_SWEEP_PIECES - 1) / KVX_SWEEP_PIECES;
     const int64_t per_slot = (int64_t)P.L * ppt;         // workgroups per page slot
     if (per_slot > KVX_SWEEP_MAX_BLOCKS) return;
     const int64_t slots = plan_pages < KVX_SWEEP_MAX_BLOCKS / per_slot ? plan_pages

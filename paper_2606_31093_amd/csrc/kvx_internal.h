@@ -15,6 +15,10 @@
 #ifndef KVX_SWEEP_MIN_BYTES
 #define KVX_SWEEP_MIN_BYTES (96 << 10)
 #endif
+// Pieces of 64 vectors one sweep workgroup copies, one after the other.
+#ifndef KVX_SWEEP_PIECES
+#define KVX_SWEEP_PIECES 1
+#endif
 // Whether planned transfers into a head-major destination sweep (the test
 // build only).
 #ifndef KVX_SWEEP_HEAD_MAJOR

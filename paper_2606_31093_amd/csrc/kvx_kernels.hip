@@ -95,6 +95,22 @@ __device__ __forceinline__ void st16(char *p, v4u v) {
     *reinterpret_cast<v4u *>(p) = v;
 }
 
+// A read of data the kernel never writes (the plan, the records, the page
+// tables) through the constant address space: the compiler may then serve a
+// uniform one from the scalar cache wherever it falls, also after stores.
+template <class T>
+__device__ __forceinline__ T cload(const T *ptr) {
+    static_assert(sizeof(T) % 4 == 0, "whole 32-bit words");
+    typedef const __attribute__((address_space(4))) uint32_t cword;
+    const cword *q = (const cword *)(uintptr_t)ptr;
+    uint32_t w[sizeof(T) / 4];
+#pragma unroll
+    for (unsigned i = 0; i < sizeof(T) / 4; ++i) w[i] = q[i];
+    T out;
+    __builtin_memcpy(&out, w, sizeof(T));
+    return out;
+}
+
 __device__ __forceinline__ void report(const Params &p, uint32_t bits) {
     if (p.err) atomicOr(p.err, bits);
 }
@@ -522,8 +538,8 @@ __device__ __forceinline__ void sweep_piece(const Params &p, const kvx_plan_slot
     const bool o_in = d.src_idx >= 0 && oidx0 < (uint32_t)os.pt_len;
     // both page ids are read before any error is reported (an atomic ahead
     // of them would turn them into vector loads)
-    const int32_t tpage = t_in ? ts.pt[(uint32_t)d.dst_idx] : -1;
-    const int32_t opage0 = t_in && one && o_in ? os.pt[oidx0] : -1;
+    const int32_t tpage = t_in ? cload(ts.pt + (uint32_t)d.dst_idx) : -1;
+    const int32_t opage0 = t_in && one && o_in ? cload(os.pt + oidx0) : -1;
     const bool pages_ok = (uint32_t)tpage < (uint32_t)ts.N && (uint32_t)opage0 < (uint32_t)os.N;
     char *t_base = ts.base + (int64_t)l * ts.s_l + (int64_t)tpage * ts.s_p;
     const char *o_l = os.base + (int64_t)l * os.s_l;
@@ -594,13 +610,17 @@ __device__ __forceinline__ bool slot_agrees(const Params &p, int64_t qi, const k
            d.src_slot == (int32_t)(pos - jo * p.src.T);
 }
 
-// Page slot qi of layer l: read its slot, copy the piece, and (one workgroup
-// per slot) check the slot against the records.
+// Page slot qi of layer l: read its slot, copy the workgroup's
+// KVX_SWEEP_PIECES pieces one after the other, and (one workgroup per slot)
+// check the slot against the records.
 template <bool TTHD, bool FLAT, bool HOST>
-__device__ __forceinline__ void sweep_slot(const Params &p, int64_t qi, uint32_t l, uint32_t piece) {
-    const kvx_plan_slot d = p.slots[qi];
-    sweep_piece<TTHD, FLAT, HOST>(p, d, l, piece * kWave);
-    if (l == 0 && piece == 0 && !slot_agrees(p, qi, d) && threadIdx.x == 0) report(p, KVX_DERR_BAD_PLAN);
+__device__ __forceinline__ void sweep_slot(const Params &p, int64_t qi, uint32_t l, uint32_t part) {
+    const kvx_plan_slot d = cload(p.slots + qi);
+    const uint32_t piece0 = part * KVX_SWEEP_PIECES;
+#pragma unroll
+    for (uint32_t i = 0; i < KVX_SWEEP_PIECES; ++i)
+        sweep_piece<TTHD, FLAT, HOST>(p, d, l, (piece0 + i) * kWave);
+    if (l == 0 && part == 0 && !slot_agrees(p, qi, d) && threadIdx.x == 0) report(p, KVX_DERR_BAD_PLAN);
 }
 
 // Sweep kernel (a planned pool -> pool transfer): one wavefront per
@@ -621,12 +641,12 @@ template <bool TTHD, bool FLAT, bool HOST>
 __global__ void __launch_bounds__(kWave) kvx_sweep_kernel(Params p) {
     const uint32_t b = blockIdx.x;
     const uint32_t slot = fd_div(p.fd_ppt, b);                 // (layer, page slot)
-    const uint32_t piece = b - slot * p.sweep_ppt;
+    const uint32_t part = b - slot * p.sweep_ppt;
     const uint32_t l = fd_div(p.fd_sp, slot);
     const int64_t q0 = (int64_t)(slot - l * (uint32_t)p.sweep_pages);
-    sweep_slot<TTHD, FLAT, HOST>(p, q0, l, piece);
+    sweep_slot<TTHD, FLAT, HOST>(p, q0, l, part);
     for (int64_t qi = q0 + p.sweep_pages; qi < p.plan_pages; qi += p.sweep_pages)  // capped launch
-        sweep_slot<TTHD, FLAT, HOST>(p, qi, l, piece);
+        sweep_slot<TTHD, FLAT, HOST>(p, qi, l, part);
     if (b == 0) {
         // prefix[0] = 0, prefix[r + 1] - prefix[r] = pages of record r, and
         // prefix[n_reqs] = plan_pages
