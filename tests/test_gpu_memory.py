@@ -1,7 +1,7 @@
-"""Where the library's inputs may live, on the GPU: page tables and request
-records in pinned host memory (read over PCIe by the kernel), the error word
-refused in pinned host memory, and descriptors larger than their allocation
-refused on the host before anything is enqueued."""
+"""Where the library's inputs may live, on the GPU: page tables, request
+records and plans in pinned host memory (read over PCIe by the kernel), the
+error word refused in pinned host memory, and descriptors larger than their
+allocation refused on the host before anything is enqueued."""
 import ctypes
 
 import numpy as np
@@ -55,6 +55,36 @@ def test_tables_and_records_in_pinned_host_memory(torch, name):
     kvx.kvx_transfer(a, S, b, D, spt, dpt, reqs, err)
     torch.cuda.synchronize()
     assert int(err.item()) == kvx.DERR_SRC_PAGE
+    assert_same({"B": b.cpu().numpy()}, {"B": want["B"]}, wl.title)
+
+
+@pytest.mark.parametrize("build", ["product", "test"])
+def test_plan_tables_and_records_in_pinned_host_memory(torch, build):
+    """A planned transfer whose plan, page tables and records are all in
+    pinned host memory gives the oracle's bytes.  256 KiB pages into a
+    token-major destination, so the product library takes the sweep; the
+    test build sweeps with a capped grid, looping over page slots."""
+    import cases
+    from paper_2606_31093_amd import build_lib, kvx
+    library = kvx.load(build_lib.TEST_LIBRARY) if build == "test" else None
+    spec = [(0, 0, 200, None), (5, 70, 333, None), (63, 1, 1, None), (0, 0, 0, None), (10, 64, 128, 0)]
+    wl = cases.transfer_case("LPCTHD", "PLCTHD", 64, 64, seed=29, e=2, D=128, L=3, C=2, H=8, spec=spec)
+    st = wl.steps[0]
+    S, D = wl.sides["A"], wl.sides["B"]
+    init = initial_bytes(wl)
+    want, werr = run_oracle(wl, init)
+    assert werr == [0]
+    a = torch.from_numpy(init["A"]).cuda()
+    b = torch.from_numpy(init["B"]).cuda()
+    buf, pages, tokens = kvx.host_plan(st.reqs, S.T, D.T)
+    plan = _pinned(torch, buf)
+    spt = _pinned(torch, st.src_pt.astype(np.int32)).view(torch.int32)
+    dpt = _pinned(torch, st.dst_pt.astype(np.int32)).view(torch.int32)
+    reqs = _pinned(torch, kvx.pack_reqs(st.reqs))
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    kvx.kvx_transfer_planned(a, S, b, D, spt, dpt, reqs, plan, pages, tokens, None, err, library=library)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
     assert_same({"B": b.cpu().numpy()}, {"B": want["B"]}, wl.title)
 
 
@@ -193,6 +223,37 @@ def test_descriptors_beyond_their_allocation_are_refused(torch):
         assert int(word[0]) == 0
     finally:
         for x in (a, b, pt, reqs, err):
+            x.free()
+
+
+def test_plan_beyond_its_allocation_is_refused(torch):
+    """A plan whose page count needs more bytes than its allocation holds is
+    refused with KVX_ERR_RANGE; the exact plan succeeds."""
+    from paper_2606_31093_amd import kvx
+    hip = _hip()
+    S = PoolSpec(1, 2, 8, 128, T=64, N=32, e=2, layout="LPCTHD")       # 8 MiB
+    rows = [[0, 0, 0, 0, 0, 256]]
+    buf, pages, tokens = kvx.host_plan(rows, S.T, S.T)
+    a, b = _Alloc(hip, S.nbytes), _Alloc(hip, S.nbytes)
+    pt = _upload(hip, np.arange(4, dtype=np.int32))
+    reqs = _upload(hip, kvx.pack_reqs(rows))
+    plan = _upload(hip, buf)
+    err = _Alloc(hip, 4)
+    assert buf.nbytes == kvx.plan_bytes(1, pages) and buf.nbytes % 16 == 0
+
+    def call(n_pages):
+        return kvx.lib().kvx_transfer_planned(ctypes.byref(kvx.pool_desc(S, a.addr)),
+                                              ctypes.byref(kvx.pool_desc(S, b.addr)), None, pt.addr, 4,
+                                              pt.addr, 4, reqs.addr, 1, plan.addr, n_pages, tokens, err.addr,
+                                              None)
+    try:
+        assert call(pages) == 0
+        torch.cuda.synchronize()
+        assert call(pages + (1 << 20)) == -5                       # 32 MiB past a 144-byte plan
+        assert "plan" in kvx.kvx_last_error() and "needs" in kvx.kvx_last_error()
+        torch.cuda.synchronize()
+    finally:
+        for x in (a, b, pt, reqs, plan, err):
             x.free()
 
 
