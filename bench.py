@@ -108,7 +108,7 @@ def parse():
                     help="most host threads for the multi-threaded oracle timing")
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
     ap.add_argument("--unplanned", action="store_true",
-                    help="launch transfers with kvx_transfer(_slice) instead of kvx_transfer_planned")
+                    help="launch transfers with kvx_transfer(_slice, _layered) instead of their planned forms")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (counter calibration)")
     return ap.parse_args()
@@ -196,7 +196,11 @@ def summary(r: dict) -> dict:
 def launch_step(kvx, wl, mem, d, errw):
     st = d["st"]
     S, D = wl.sides[st.src], wl.sides[st.dst]
-    if st.op == "transfer" and d.get("plan") is not None:
+    if st.op == "transfer" and d.get("plan") is not None and st.layer_group:
+        kvx.kvx_transfer_layered_planned(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
+                                         st.layer_group, d["events"], d["plan"], d["plan_pages"],
+                                         d["plan_tokens"], st.slice, errw)
+    elif st.op == "transfer" and d.get("plan") is not None:
         kvx.kvx_transfer_planned(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
                                  d["plan"], d["plan_pages"], d["plan_tokens"], st.slice, errw)
     elif st.op == "transfer" and st.layer_group:
@@ -250,7 +254,7 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
             # and uploaded with them (kvx_transfer_planned)
             **(dict(zip(("plan", "plan_pages", "plan_tokens"),
                         kvx.device_plan(st.reqs, wl.sides[st.src].T, wl.sides[st.dst].T, dev)))
-               if st.op == "transfer" and not st.layer_group and not args.unplanned else {})))
+               if st.op == "transfer" and not args.unplanned else {})))
     errw = torch.zeros(1, dtype=torch.int32, device=dev)
     torch.cuda.synchronize()
 

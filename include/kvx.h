@@ -333,6 +333,19 @@ int kvx_transfer_planned(const kvx_pool *src, const kvx_pool *dst, const kvx_sli
                          const void *plan, int64_t plan_pages, int64_t plan_tokens,
                          uint32_t *dev_err, void *stream);
 
+/* kvx_transfer_layered with a plan: each layer group's launch is that of
+ * kvx_transfer_planned over the group's layers (the plan describes pages,
+ * so one plan serves every group).  Arguments, events and rules are those
+ * of kvx_transfer_layered and kvx_transfer_planned; the plan is checked
+ * against the records in every group's launch. */
+int kvx_transfer_layered_planned(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                                 const int32_t *src_pt, int64_t src_pt_len,
+                                 const int32_t *dst_pt, int64_t dst_pt_len,
+                                 const kvx_req *reqs, int32_t n_reqs,
+                                 int32_t layers_per_group, void *const *events, int32_t n_events,
+                                 const void *plan, int64_t plan_pages, int64_t plan_tokens,
+                                 uint32_t *dev_err, void *stream);
+
 /* Sizes a plan from a host copy of the records: writes the exclusive prefix
  * of pages per record into prefix[0..n_reqs] and the tokens of the
  * well-formed records into *tokens (each if not NULL), and returns the

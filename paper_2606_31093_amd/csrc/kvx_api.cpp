@@ -424,7 +424,7 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
             P.dst = pool_side(dst, v.dst, v.dst_pt, dst_pt_len, sl.dst_layer0 + l0, sl.dst_kv0,
                               sl.dst_head0, sl.num_heads);
             finish_params(P, Shape{nl, sl.num_kv, sl.num_heads, ss.D, ss.e}, v, n_reqs);
-            if (group == 0) plan_sweep(P, plan, plan_pages, plan_tokens);
+            plan_sweep(P, plan, plan_pages, plan_tokens);
             if ((st = enqueue(P, stream))) return st;
         }
         if (group > 0) {
@@ -588,6 +588,25 @@ int kvx_transfer_planned(const kvx_pool *src, const kvx_pool *dst, const kvx_sli
     if ((reinterpret_cast<uintptr_t>(plan) & 7u) != 0) return fail(KVX_ERR_ALIGN, "plan is not 8-byte aligned");
     return transfer_impl(src, dst, slice, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
                          dev_err, stream, 0, nullptr, 0, plan, plan_pages, plan_tokens);
+}
+
+int kvx_transfer_layered_planned(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
+                                 const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
+                                 int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs,
+                                 int32_t layers_per_group, void *const *events, int32_t n_events,
+                                 const void *plan, int64_t plan_pages, int64_t plan_tokens,
+                                 uint32_t *dev_err, void *stream) {
+    g_last_error.clear();
+    if (layers_per_group < 1)
+        return fail(KVX_ERR_RANGE, "layers_per_group must be >= 1 (got %d)", layers_per_group);
+    if (plan_pages < 0 || plan_tokens < 0 || plan_pages > (int64_t)KVX_MAX_REQS * INT32_MAX)
+        return fail(KVX_ERR_RANGE, "plan_pages and plan_tokens must be >= 0 (got %lld, %lld)",
+                    (long long)plan_pages, (long long)plan_tokens);
+    if (n_reqs > 0 && !plan) return fail(KVX_ERR_NULL, "plan is NULL");
+    if ((reinterpret_cast<uintptr_t>(plan) & 7u) != 0) return fail(KVX_ERR_ALIGN, "plan is not 8-byte aligned");
+    return transfer_impl(src, dst, slice, src_pt, src_pt_len, dst_pt, dst_pt_len, reqs, n_reqs,
+                         dev_err, stream, layers_per_group, events, n_events, plan, plan_pages,
+                         plan_tokens);
 }
 
 int64_t kvx_plan_pages(const kvx_req *host_reqs, int32_t n_reqs, int32_t page_tokens, int32_t side,

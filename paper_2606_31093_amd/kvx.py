@@ -4,9 +4,10 @@ Every step of the copy runs in the library's HIP kernels.  PyTorch supplies
 device memory and the stream: tensors are passed as raw pointers and the
 kernels run on ``torch.cuda.current_stream()`` unless a stream is given.
 The functions keep the C names: ``kvx_transfer``, ``kvx_transfer_slice``,
-``kvx_transfer_layered``, ``kvx_transfer_planned``, ``kvx_gather``, ``kvx_scatter``,
-``kvx_gather_slice``, ``kvx_scatter_slice`` and ``kvx_page_hashes``.  A missing or unloadable library raises; there is no
-fallback path.
+``kvx_transfer_layered``, ``kvx_transfer_planned``,
+``kvx_transfer_layered_planned``, ``kvx_gather``, ``kvx_scatter``,
+``kvx_gather_slice``, ``kvx_scatter_slice`` and ``kvx_page_hashes``.  A
+missing or unloadable library raises; there is no fallback path.
 
 Pool and buffer shapes are duck-typed: a pool shape has integer attributes
 ``L C H D T N e`` and a ``layout`` name; a buffer shape has ``L C H D e``
@@ -128,6 +129,9 @@ def load(path: str) -> ctypes.CDLL:
     L.kvx_transfer_planned.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp, i32,
                                        vp, i64, i64, vp, vp]
     L.kvx_transfer_planned.restype = ctypes.c_int
+    L.kvx_transfer_layered_planned.argtypes = [pp, pp, ctypes.POINTER(Slice), vp, i64, vp, i64, vp,
+                                               i32, i32, ctypes.POINTER(vp), i32, vp, i64, i64, vp, vp]
+    L.kvx_transfer_layered_planned.restype = ctypes.c_int
     L.kvx_plan_pages.argtypes = [vp, i32, i32, i32, vp, vp]
     L.kvx_plan_pages.restype = ctypes.c_int64
     L.kvx_plan_fill.argtypes = [vp, i32, i32, i32, i64, vp]
@@ -372,17 +376,10 @@ def device_plan(rows, src_page_tokens: int, dst_page_tokens: int, device="cuda")
     return torch.from_numpy(buf).to(device), pages, tokens
 
 
-def kvx_transfer_layered(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, layers_per_group,
-                         events, sl=None, dev_err=None, stream=None) -> None:
-    """Layer-pipelined pool -> pool (see kvx_transfer_layered in
-    include/kvx.h).  ``events`` are ``torch.cuda.Event`` objects (or raw
-    hipEvent_t handles), one per layer group; the library records events[g]
-    on the stream once group g has been copied."""
+def _event_handles(events, st, stream):
+    """hipEvent_t handles of ``events`` (torch.cuda.Event objects or raw
+    handles) as a ctypes array, and their count."""
     import torch
-    _need(src, _pool_nbytes(src_spec), "src")
-    _need(dst, _pool_nbytes(dst_spec), "dst")
-    _table(src_pt, "src_pt"), _table(dst_pt, "dst_pt"), _err_word(dev_err)
-    st = _stream(stream)
     handles = []
     for ev in events:
         if isinstance(ev, int):
@@ -391,13 +388,52 @@ def kvx_transfer_layered(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, lay
         if not ev.cuda_event:          # torch creates the HIP event on first record
             ev.record(torch.cuda.ExternalStream(st) if stream is not None else None)
         handles.append(ev.cuda_event)
-    arr = (ctypes.c_void_p * max(1, len(handles)))(*handles)
+    return (ctypes.c_void_p * max(1, len(handles)))(*handles), len(handles)
+
+
+def kvx_transfer_layered(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, layers_per_group,
+                         events, sl=None, dev_err=None, stream=None) -> None:
+    """Layer-pipelined pool -> pool (see kvx_transfer_layered in
+    include/kvx.h).  ``events`` are ``torch.cuda.Event`` objects (or raw
+    hipEvent_t handles), one per layer group; the library records events[g]
+    on the stream once group g has been copied."""
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    _table(src_pt, "src_pt"), _table(dst_pt, "dst_pt"), _err_word(dev_err)
+    st = _stream(stream)
+    arr, n_ev = _event_handles(events, st, stream)
     S, D = pool_desc(src_spec, src), pool_desc(dst_spec, dst)
     X = None if sl is None else ctypes.byref(slice_desc(sl))
     _check(lib().kvx_transfer_layered(ctypes.byref(S), ctypes.byref(D), X, _ptr(src_pt),
                                       _len(src_pt), _ptr(dst_pt), _len(dst_pt), _ptr(reqs),
-                                      _n_reqs(reqs), int(layers_per_group), arr, len(handles),
+                                      _n_reqs(reqs), int(layers_per_group), arr, n_ev,
                                       _ptr(dev_err), st))
+
+
+def kvx_transfer_layered_planned(src, src_spec, dst, dst_spec, src_pt, dst_pt, reqs, layers_per_group,
+                                 events, plan, plan_pages, plan_tokens, sl=None, dev_err=None,
+                                 stream=None, library=None) -> None:
+    """kvx_transfer_layered with a plan (see kvx_transfer_layered_planned
+    in include/kvx.h); the plan as ``device_plan`` returns it."""
+    _need(src, _pool_nbytes(src_spec), "src")
+    _need(dst, _pool_nbytes(dst_spec), "dst")
+    _table(src_pt, "src_pt"), _table(dst_pt, "dst_pt"), _err_word(dev_err)
+    n = _n_reqs(reqs)
+    if plan is not None and not isinstance(plan, int):
+        if not plan.is_contiguous() or plan.numel() * plan.element_size() < plan_bytes(n, plan_pages):
+            raise ValueError("plan must be a contiguous tensor of KVX_PLAN_BYTES(n_reqs, plan_pages) "
+                             "bytes")
+    st = _stream(stream)
+    arr, n_ev = _event_handles(events, st, stream)
+    S, D = pool_desc(src_spec, src), pool_desc(dst_spec, dst)
+    X = None if sl is None else ctypes.byref(slice_desc(sl))
+    L = library or lib()
+    status = L.kvx_transfer_layered_planned(ctypes.byref(S), ctypes.byref(D), X, _ptr(src_pt),
+                                            _len(src_pt), _ptr(dst_pt), _len(dst_pt), _ptr(reqs), n,
+                                            int(layers_per_group), arr, n_ev, _ptr(plan),
+                                            int(plan_pages), int(plan_tokens), _ptr(dev_err), st)
+    if status != 0:
+        raise KvxError(status, L.kvx_last_error().decode())
 
 
 def kvx_gather(src, src_spec, dst, buf_spec, src_pt, reqs, dev_err=None, stream=None) -> None:

@@ -88,8 +88,15 @@ def run_gpu(wl, init: dict, raw_reqs=None, planned=None, library=None) -> tuple[
         elif st.op == "transfer" and st.layer_group:
             n_layers = st.slice[2] if st.slice is not None else S.L
             events = [torch.cuda.Event() for _ in range(-(-n_layers // st.layer_group))]
-            kvx.kvx_transfer_layered(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs,
-                                     st.layer_group, events, st.slice, err)
+            if planned is not None:
+                buf, pages, tokens = planned(*kvx.host_plan(
+                    raw_reqs[i] if raw_reqs is not None else st.reqs, S.T, D.T))
+                kvx.kvx_transfer_layered_planned(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs,
+                                                 st.layer_group, events, torch.from_numpy(buf).to(dev),
+                                                 pages, tokens, st.slice, err, library=library)
+            else:
+                kvx.kvx_transfer_layered(mem[st.src], S, mem[st.dst], D, spt, dpt, reqs,
+                                         st.layer_group, events, st.slice, err)
         elif st.op == "transfer" and st.slice is not None:
             kvx.kvx_transfer_slice(mem[st.src], S, mem[st.dst], D, st.slice, spt, dpt, reqs, err)
         elif st.op == "transfer":

@@ -552,6 +552,22 @@ def test_planned_transfer_host_validation(lib):
     assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 0, None, 0, 0, None, None) == 0   # nothing to do
 
 
+def test_layered_planned_transfer_host_validation(lib):
+    """The layered planned transfer checks the group size and the plan
+    arguments, then the plain layered transfer's rules."""
+    S = PoolSpec(2, 2, 1, 8, T=4, N=4, e=2, layout="LPCTHD")
+    P = ctypes.byref(kvx.pool_desc(S, FAKE))
+    ev = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    call = lib.kvx_transfer_layered_planned
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, 0, ev, 2, FAKE, 3, 4, None, None) == -5
+    assert "layers_per_group" in kvx.kvx_last_error()
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, 1, ev, 2, FAKE, -1, 4, None, None) == -5
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, 1, ev, 2, None, 3, 4, None, None) == -1
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, 1, ev, 2, FAKE + 4, 3, 4, None, None) == -3
+    assert call(P, P, None, FAKE, 4, FAKE, 4, FAKE, 1, 1, ev, 1, FAKE, 3, 4, None, None) == -5
+    assert "events" in kvx.kvx_last_error()
+
+
 def test_test_build_exports_the_same_functions():
     out = subprocess.run(["nm", "-D", "--defined-only", build_lib.TEST_LIBRARY], capture_output=True,
                          text=True, check=True).stdout

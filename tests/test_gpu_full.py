@@ -48,7 +48,13 @@ def _run(torch, wl, mem, d, planned=True):
     st = d["st"]
     err = torch.zeros(1, dtype=torch.int32, device="cuda")
     S, D = wl.sides[st.src], wl.sides[st.dst]
-    if st.op == "transfer" and planned:
+    if st.op == "transfer" and planned and st.layer_group:
+        plan, pages, tokens = kvx.device_plan(st.reqs, S.T, D.T)
+        n_layers = st.slice[2] if st.slice is not None else S.L
+        events = [torch.cuda.Event() for _ in range(-(-n_layers // st.layer_group))]
+        kvx.kvx_transfer_layered_planned(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
+                                         st.layer_group, events, plan, pages, tokens, st.slice, err)
+    elif st.op == "transfer" and planned:
         plan, pages, tokens = kvx.device_plan(st.reqs, S.T, D.T)
         kvx.kvx_transfer_planned(mem[st.src], S, mem[st.dst], D, d["spt"], d["dpt"], d["reqs"],
                                  plan, pages, tokens, st.slice, err)
@@ -80,9 +86,9 @@ def _free(torch, *objs):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("k,planned", [("handoff", True), ("handoff", False), ("relayout", True),
-                                     ("mla", True), ("tp_reshard", True), ("cow_fork", True),
-                                     ("small_requests", True)])
+@pytest.mark.parametrize("k,planned", [("handoff", True), ("handoff", False), ("handoff_layered", True),
+                                       ("relayout", True), ("mla", True), ("tp_reshard", True),
+                                       ("cow_fork", True), ("small_requests", True)])
 def test_full_transfer(torch, k, planned):
     from oracle import layer_check
     wl, mem, dsteps = _setup(torch, k)

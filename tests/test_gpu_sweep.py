@@ -122,6 +122,44 @@ def test_device_errors(test_lib, src_pt, dst_pt, row):
     check(_err_wl(src_pt, dst_pt, [row, [0, 0, 0, 0, 0, 2]]), test_lib)
 
 
+@pytest.mark.parametrize("group", [1, 2, 3, 5])
+@pytest.mark.parametrize("with_slice", [False, True])
+def test_layered(test_lib, group, with_slice):
+    """kvx_transfer_layered_planned: one sweep launch per layer group."""
+    if with_slice:
+        wl = cases.slice_case("LPCTHD", "PLCHTD", 4, 8, (5, 2, 4), (4, 2, 2),
+                              (1, 0, 4, 0, 0, 2, 2, 0, 2), seed=group)
+    else:
+        wl = cases.transfer_case("LPCHTD", "LPCTHD", 16, 32, seed=group, L=5)
+    wl.steps[0].layer_group = group
+    check(wl, test_lib)
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_layered_cases(test_lib, seed):
+    check(cases.random_layered_case(seed), test_lib, list(TOKENS)[seed % len(TOKENS)])
+
+
+def test_layered_plan_that_disagrees_is_reported(test_lib):
+    import torch
+    from paper_2606_31093_amd import kvx
+    wl = cases.transfer_case("LPCTHD", "LPCTHD", 4, 8, seed=23, L=4)
+    st = wl.steps[0]
+    S, D = wl.sides["A"], wl.sides["B"]
+    init = initial_bytes(wl)
+    a, b = torch.from_numpy(init["A"]).cuda(), torch.from_numpy(init["B"]).cuda()
+    buf, pages, tokens = kvx.host_plan(st.reqs, S.T, D.T)
+    kvx.plan_slots(buf, len(st.reqs))[1, 2] += 1          # one slot's first destination slot
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    events = [torch.cuda.Event() for _ in range(2)]
+    kvx.kvx_transfer_layered_planned(a, S, b, D, kvx.device_table(st.src_pt), kvx.device_table(st.dst_pt),
+                                     kvx.device_reqs(st.reqs), 2, events, torch.from_numpy(buf).cuda(),
+                                     pages, tokens, None, err, library=test_lib)
+    torch.cuda.synchronize()
+    assert int(err.item()) & kvx.DERR_BAD_PLAN
+    assert all(ev.query() for ev in events)
+
+
 def test_many_records(test_lib):
     """300 records, some empty."""
     spec = [(i % 5, (i * 3) % 7, 0 if i % 17 == 0 else 1 + (i * 13) % 40, None) for i in range(300)]
