@@ -154,7 +154,6 @@ __device__ __forceinline__ bool load_req(const Params &p, int32_t r, Req &q) {
     q.o_start = tsrc ? d0 : s0;
     q.n = n;
     q.blk = bo * p.elem_bytes;
-    const Side &ts = tsrc ? p.src : p.dst;
     if (n == 0) {
         q.tiles = 0;
         q.pages = 0;
