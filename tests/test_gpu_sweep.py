@@ -12,7 +12,7 @@ launch.  A plan that disagrees with the records (a wrong page total, a
 damaged prefix or slot, slots out of order, page sizes of other pools, or
 random slot contents) raises KVX_DERR_BAD_PLAN, and every access still
 stays inside the pools and tables.  The product library sweeps when the
-records copy 96 KiB or more per page on average into a token-major
+records copy 64 KiB or more per page on average into a token-major
 destination; a shape with 256 KiB pages checks it there, and the full-size
 handoff is checked on every layer in test_gpu_full."""
 import numpy as np
