@@ -253,6 +253,42 @@ def test_random_slots_stay_in_bounds(test_lib, seed):
     assert _bad_plan_run(test_lib, alter) & kvx.DERR_BAD_PLAN
 
 
+def test_graph_replays_of_the_product_sweep():
+    """A planned transfer the product library sweeps (256 KiB pages),
+    captured in a HIP graph and replayed three times with eager work in
+    between, gives the oracle's bytes and no error bit every time."""
+    import torch
+    from paper_2606_31093_amd import kvx
+    spec = [(0, 0, 200, None), (5, 70, 333, None), (63, 1, 1, None), (10, 64, 128, 0)]
+    wl = cases.transfer_case("LPCTHD", "PLCTHD", 64, 64, seed=31, e=2, D=128, L=3, C=2, H=8, spec=spec)
+    st = wl.steps[0]
+    S, D = wl.sides["A"], wl.sides["B"]
+    init = initial_bytes(wl)
+    want, _ = run_oracle(wl, init)
+    a, b = torch.from_numpy(init["A"]).cuda(), torch.from_numpy(init["B"]).cuda()
+    b0 = b.clone()
+    spt, dpt, reqs = kvx.device_table(st.src_pt), kvx.device_table(st.dst_pt), kvx.device_reqs(st.reqs)
+    plan, pages, tokens = kvx.device_plan(st.reqs, S.T, D.T)
+    err = torch.zeros(1, dtype=torch.int32, device="cuda")
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        kvx.kvx_transfer_planned(a, S, b, D, spt, dpt, reqs, plan, pages, tokens, None, err, stream=s)
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        kvx.kvx_transfer_planned(a, S, b, D, spt, dpt, reqs, plan, pages, tokens, None, err)
+    for _ in range(3):
+        b.copy_(b0)                    # eager work between replays
+        err.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert int(err.item()) == 0
+        assert np.array_equal(b.cpu().numpy(), want["B"])
+
+
 @pytest.mark.parametrize("tokens", ["true", "double"])
 @pytest.mark.parametrize("ls,ld", [("LPCTHD", "LPCTHD"), ("PLCHTD", "PLCTHD"), ("LPCTHD", "PLCHTD")])
 def test_product_library_sweeps_large_tiles(ls, ld, tokens):
