@@ -486,12 +486,12 @@ __device__ __forceinline__ void tile_row(const Params &p, uint32_t k, uint32_t r
 // lie in one source page, the usual case) is uniform and comes before the
 // first store or atomic, so it goes through the scalar cache.  FLAT (both
 // sides token-major with every head): the page is C runs of contiguous
-// vectors on both sides, the piece's source pages are found from its first
-// and last vectors, and a piece in one source page is a plain vector copy.
-// Errors are reported for the positions the piece covers, destination
-// first.  The slot's fields are only trusted as far as keeping every access
-// inside the pools and tables; whether they match the records is checked
-// separately (check_slot).
+// vectors on both sides, each lane finds its token's source page, and a
+// piece whose rows lie in one source page is a plain vector copy.  Errors
+// are reported for the positions the piece covers, destination first.  The
+// slot's fields are only trusted as far as keeping every access inside the
+// pools and tables; whether they match the records is checked separately
+// (slot_agrees).
 template <bool TTHD, bool FLAT, bool HOST>
 __device__ __forceinline__ void sweep_piece(const Params &p, const kvx_plan_slot &d, uint32_t l,
                                             uint32_t kb) {
