@@ -130,7 +130,7 @@ def calibrate_copy(gib: float) -> None:
 def main() -> int:
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "kvx is measured on one GPU; this build has no multi-GPU path, "
+        print(json.dumps({"error": "kvx is measured on one GPU; the library has no multi-GPU path, "
                                    "so --gpus must be 1", "n_gpus": args.gpus}), flush=True)
         return 2
     if int(os.environ.get("WORLD_SIZE", "1")) != 1:
