@@ -385,3 +385,25 @@ def random_layered_case(seed: int) -> Workload:
 
 RANDOM_COW_CASES = 40
 RANDOM_LAYERED_CASES = 40
+
+
+def random_planned_medium_case(seed: int) -> Workload:
+    """A seeded medium transfer whose token-major destination pages hold 128
+    or 256 KiB (so a planned call sweeps in the product library too): 8-39
+    requests of up to 399 tokens, any source layout, 16-64-token source
+    pages, some requests reading an earlier request's source pages."""
+    rng = np.random.default_rng(90_000 + seed)
+    pick = lambda xs: xs[int(rng.integers(len(xs)))]
+    ls, ld = pick(["LPCTHD", "LPCHTD", "PLCTHD", "PLCHTD"]), pick(["LPCTHD", "PLCTHD"])
+    Ts, Td = pick([16, 32, 64]), 64
+    spec = []
+    for r in range(int(rng.integers(8, 40))):
+        n = 0 if rng.random() < 0.05 else int(rng.integers(1, 400))
+        share = int(rng.integers(0, r)) if r > 0 and rng.random() < 0.1 else None
+        s0 = int(rng.integers(0, 2 * Ts)) if share is None else 0
+        d0 = int(rng.integers(0, 2 * Td))
+        if share is not None:                    # stay inside the pages it reads
+            n = min(n, spec[share][0] + spec[share][2])
+        spec.append((s0, d0, n, share))
+    return transfer_case(ls, ld, Ts, Td, seed=90_000 + seed, e=2, D=128, L=int(rng.integers(1, 4)), C=2,
+                         H=pick([4, 8]), spec=spec)

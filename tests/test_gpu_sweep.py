@@ -253,6 +253,15 @@ def test_random_slots_stay_in_bounds(test_lib, seed):
     assert _bad_plan_run(test_lib, alter) & kvx.DERR_BAD_PLAN
 
 
+@pytest.mark.parametrize("seed", range(20))
+def test_random_medium_cases(test_lib, seed):
+    """Medium transfers with 128-256 KiB token-major destination pages,
+    through the product library (which sweeps them) and the test build."""
+    wl = cases.random_planned_medium_case(seed)
+    check(wl, None)
+    check(wl, test_lib)
+
+
 def test_graph_replays_of_the_product_sweep():
     """A planned transfer the product library sweeps (256 KiB pages),
     captured in a HIP graph and replayed three times with eager work in
