@@ -358,8 +358,9 @@ void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t pl
     const int64_t ppt = ((tile_vecs + 63) / 64 + KVX_SWEEP_PIECES - 1) / KVX_SWEEP_PIECES;
     const int64_t per_slot = (int64_t)P.L * ppt;         // workgroups per page slot
     if (per_slot > KVX_SWEEP_MAX_BLOCKS) return;
-    const int64_t slots = plan_pages < KVX_SWEEP_MAX_BLOCKS / per_slot ? plan_pages
-                                                                      : KVX_SWEEP_MAX_BLOCKS / per_slot;
+    // page slots per pass: the plan's pages in KVX_SWEEP_PASSES passes, within the grid cap
+    const int64_t want = (plan_pages + KVX_SWEEP_PASSES - 1) / KVX_SWEEP_PASSES;
+    const int64_t slots = want < KVX_SWEEP_MAX_BLOCKS / per_slot ? want : KVX_SWEEP_MAX_BLOCKS / per_slot;
     P.sweep = 1;
     P.prefix = static_cast<const int64_t *>(plan);
     P.slots = reinterpret_cast<const kvx_plan_slot *>(P.prefix + P.n_reqs + 1);

@@ -20,6 +20,12 @@
 #ifndef KVX_SWEEP_PIECES
 #define KVX_SWEEP_PIECES 1
 #endif
+// Passes of a sweep launch over the plan's pages: each workgroup copies its
+// piece of one page in each pass, pages plan_pages / passes apart (measured:
+// 3 passes move 256 KiB pages 7% faster than 1, and 72 KiB pages within 1%).
+#ifndef KVX_SWEEP_PASSES
+#define KVX_SWEEP_PASSES 3
+#endif
 // Whether planned transfers into a head-major destination sweep (the test
 // build only).
 #ifndef KVX_SWEEP_HEAD_MAJOR
@@ -93,11 +99,12 @@ struct Params {
     FastDiv fd_vpr, fd_H, fd_To;
     FastDiv fd_Tt;       // tiling side's page_tokens
     // Sweep launch (a planned pool -> pool transfer): one workgroup per piece
-    // of 64 vectors of one destination page of one layer.  sweep_pages page
-    // slots per layer are launched (at most plan_pages; workgroups go on to
-    // the slots sweep_pages apart when the launch is capped), sweep_ppt
-    // pieces per page.  prefix[r] = destination pages of records 0..r-1,
-    // slots[q] = page q of the plan.  sweep == 0: persistent grid.
+    // of 64 vectors of one destination page of one layer and pass.
+    // sweep_pages page slots per layer are launched (plan_pages / passes, or
+    // fewer when the grid is capped; workgroups go on to the slots
+    // sweep_pages apart), sweep_ppt pieces per page.  prefix[r] =
+    // destination pages of records 0..r-1, slots[q] = page q of the plan.
+    // sweep == 0: persistent grid.
     int32_t sweep;
     int32_t sweep_pages;
     uint32_t sweep_ppt;

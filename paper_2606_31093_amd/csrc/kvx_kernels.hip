@@ -624,18 +624,20 @@ __device__ __forceinline__ void sweep_slot(const Params &p, int64_t qi, uint32_t
 
 // Sweep kernel (a planned pool -> pool transfer): one wavefront per
 // workgroup, and workgroup b copies one piece of 64 vectors (1 KiB) of one
-// destination page of one layer, found by one read of the plan.  Workgroups
-// are numbered layer by layer, page by page within a layer (pages in plan
-// order), piece by piece within a page, so the hardware dispatcher, which
-// starts them in order, keeps the pieces in flight on the whole GPU inside a
-// small window that slides through the transfer.  (A persistent grid lets
-// its workers drift over the whole transfer; on the same pools this order
-// moves 10-20% more bytes per second for 256 KiB pages.)  The launch has
-// layers x sweep_pages x ppt workgroups; when sweep_pages is below
-// plan_pages (a capped launch), workgroups go on to the slots sweep_pages
-// apart.  The first slot is taken outside that loop, so that its loads
-// precede every store of the kernel.  Workgroup 0 finally checks the
-// prefix against the records and plan_pages, and reports malformed records.
+// destination page of one layer in each pass, found by one read of the
+// plan.  Workgroups are numbered layer by layer, page slot by page slot
+// within a layer (pages in plan order), piece by piece within a page, so the
+// hardware dispatcher, which starts them in order, keeps the pieces in
+// flight on the whole GPU inside a small window that slides through the
+// transfer.  (A persistent grid lets its workers drift over the whole
+// transfer; on the same pools this order moves up to 20% more bytes per
+// second for 256 KiB pages.)  The launch has layers x sweep_pages x ppt
+// workgroups, with sweep_pages about plan_pages / KVX_SWEEP_PASSES (fewer
+// when the grid is capped): each workgroup goes on to the slots
+// sweep_pages apart, up to plan_pages.  The first slot is taken outside that
+// loop, so that its loads precede every store of the kernel.  Workgroup 0
+// finally checks the prefix against the records and plan_pages, and reports
+// malformed records.
 template <bool TTHD, bool FLAT, bool HOST>
 __global__ void __launch_bounds__(kWave) kvx_sweep_kernel(Params p) {
     const uint32_t b = blockIdx.x;
@@ -644,7 +646,7 @@ __global__ void __launch_bounds__(kWave) kvx_sweep_kernel(Params p) {
     const uint32_t l = fd_div(p.fd_sp, slot);
     const int64_t q0 = (int64_t)(slot - l * (uint32_t)p.sweep_pages);
     sweep_slot<TTHD, FLAT, HOST>(p, q0, l, part);
-    for (int64_t qi = q0 + p.sweep_pages; qi < p.plan_pages; qi += p.sweep_pages)  // capped launch
+    for (int64_t qi = q0 + p.sweep_pages; qi < p.plan_pages; qi += p.sweep_pages)  // later passes
         sweep_slot<TTHD, FLAT, HOST>(p, qi, l, part);
     if (b == 0) {
         // prefix[0] = 0, prefix[r + 1] - prefix[r] = pages of record r, and
