@@ -314,7 +314,7 @@ typedef struct kvx_plan_slot {
  * by layer and page by page, instead of a persistent grid.  Started in that
  * order by the hardware, the pieces in flight stay within a small window
  * that slides through the transfer; on MI355X this holds the handoff's 256
- * KiB pages at 6.0-6.15 TB/s and MLA's 72 KiB pages at 5.65-5.8 TB/s in
+ * KiB pages at 6.0-6.2 TB/s and MLA's 72 KiB pages at 5.6-5.8 TB/s in
  * every process, where the persistent grid ranges from 5.1 to 6.4 TB/s with
  * the physical placement of the pools.
  * Otherwise the call runs as the unplanned one and the plan is not read.

@@ -12,7 +12,8 @@
 #endif
 // A planned transfer sweeps when its records copy at least this many bytes
 // per destination page and layer on average (measured: from 72 KiB pages up
-// the sweep holds 71-77% of HBM peak in every placement of the pools).
+// the sweep holds its rate in every placement of the pools, where the
+// persistent grid's varies by up to 15%).
 #ifndef KVX_SWEEP_MIN_BYTES
 #define KVX_SWEEP_MIN_BYTES (64 << 10)
 #endif
