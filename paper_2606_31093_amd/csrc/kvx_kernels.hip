@@ -630,7 +630,7 @@ __device__ __forceinline__ void sweep_slot(const Params &p, int64_t qi, uint32_t
 // hardware dispatcher, which starts them in order, keeps the pieces in
 // flight on the whole GPU inside a small window that slides through the
 // transfer.  (A persistent grid lets its workers drift over the whole
-// transfer; on the same pools this order moves up to 20% more bytes per
+// transfer; on the same pools this order moves up to 16% more bytes per
 // second for 256 KiB pages.)  The launch has layers x sweep_pages x ppt
 // workgroups, with sweep_pages about plan_pages / KVX_SWEEP_PASSES (fewer
 // when the grid is capped): each workgroup goes on to the slots
