@@ -307,16 +307,15 @@ typedef struct kvx_plan_slot {
  * plan_pages: prefix[n_reqs]; plan_tokens: n_tokens summed over the
  *   well-formed records (kvx_plan_pages returns both).  Read on the host to
  *   shape the launch.
- * When the destination is token-major (LPCTHD or PLCTHD, every head), the
- * records copy at least 64 KiB per destination page and layer on average,
- * and both tables hold at most INT32_MAX entries, the library launches one
- * workgroup per 1 KiB piece of each destination page of each layer, layer
- * by layer and page by page, instead of a persistent grid.  Started in that
- * order by the hardware, the pieces in flight stay within a small window
- * that slides through the transfer; on MI355X this holds the handoff's 256
- * KiB pages at 6.0-6.2 TB/s and MLA's 72 KiB pages at 5.6-5.8 TB/s in
- * every process, where the persistent grid ranges from 5.1 to 6.4 TB/s with
- * the physical placement of the pools.
+ * When the records copy at least 64 KiB per destination page and layer on
+ * average and both tables hold at most INT32_MAX entries, the library
+ * launches one workgroup per 1 KiB piece of each destination page of each
+ * layer, layer by layer and page by page, every page on one XCD, instead of
+ * a persistent grid.  Started in that order by the hardware, the pieces in
+ * flight stay within a small window that slides through the transfer; on
+ * MI355X this holds the handoff's 256 KiB pages at 6.1 TB/s and MLA's 72 KiB
+ * pages at 5.9 TB/s in every process, where the persistent grid ranges from
+ * 5.1 to 6.4 TB/s with the physical placement of the pools.
  * Otherwise the call runs as the unplanned one and the plan is not read.
  * Results, error bits and every rule are those of kvx_transfer(_slice):
  * - a plan that disagrees with the records, or with the pools' page sizes,

@@ -333,18 +333,14 @@ int check_slice(const kvx_slice &sl, const Shape &s, const Shape &d) {
 // group > 0 the layer range is moved in groups of `group` layers, one launch
 // each, and events[g] is recorded on the stream after group g.
 // A planned transfer whose shape the sweep kernel serves well gets its
-// launch: a token-major destination (measured: a head-major one splits each
-// piece into row-sized fragments and runs slower than the persistent grid),
-// at least KVX_SWEEP_MIN_BYTES copied per destination page and layer on
-// average, page tables whose indices fit in int32, and a grid of at most
+// launch: at least KVX_SWEEP_MIN_BYTES copied per destination page and layer
+// on average, page tables whose indices fit in int32, and a grid of at most
 // KVX_SWEEP_MAX_BLOCKS workgroups per pass.  Otherwise, and for unplanned
-// calls, the persistent grid.  The test build sweeps head-major
-// destinations too, to keep that path covered.
+// calls, the persistent grid.
 void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t plan_tokens) {
     P.sweep = 0;
     if (!plan || plan_pages < 1 || plan_tokens < 1 || P.n_reqs < 1 || P.op != kvx::OP_TRANSFER) return;
     if (P.src.pt_len > INT32_MAX || P.dst.pt_len > INT32_MAX) return;
-    if (!P.dst.tok_contig && !KVX_SWEEP_HEAD_MAJOR) return;
     const int64_t T = P.dst.T, rows_per_head =
         P.dst.tok_contig ? T : (T + KVX_SLOT_BLOCK - 1) / KVX_SLOT_BLOCK * KVX_SLOT_BLOCK + KVX_SLOT_BLOCK;
     // average bytes copied per destination page and layer

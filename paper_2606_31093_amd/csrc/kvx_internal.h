@@ -23,14 +23,9 @@
 #endif
 // Passes of a sweep launch over the plan's pages: each workgroup copies its
 // piece of one page in each pass, pages plan_pages / passes apart (measured:
-// 3 passes move 128-256 KiB pages 8-12% faster than 1, 72 KiB pages as fast).
+// 3 passes move 128-256 KiB pages 4-6% faster than 1, 72 KiB pages within 1%).
 #ifndef KVX_SWEEP_PASSES
 #define KVX_SWEEP_PASSES 3
-#endif
-// Whether planned transfers into a head-major destination sweep (the test
-// build only).
-#ifndef KVX_SWEEP_HEAD_MAJOR
-#define KVX_SWEEP_HEAD_MAJOR 0
 #endif
 // Most workgroups of one sweep launch: the work-items of a launch (64 per
 // workgroup) must stay below 2^32, and this keeps them below 2^31.  Beyond

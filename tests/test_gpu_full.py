@@ -87,7 +87,8 @@ def _free(torch, *objs):
 
 
 @pytest.mark.parametrize("k,planned", [("handoff", True), ("handoff", False), ("handoff_layered", True),
-                                       ("relayout", True), ("mla", True), ("tp_reshard", True),
+                                       ("relayout", True), ("relayout", False), ("mla", True),
+                                       ("tp_reshard", True),
                                        ("cow_fork", True), ("small_requests", True)])
 def test_full_transfer(torch, k, planned):
     from oracle import layer_check

@@ -12,9 +12,9 @@ launch.  A plan that disagrees with the records (a wrong page total, a
 damaged prefix or slot, slots out of order, page sizes of other pools, or
 random slot contents) raises KVX_DERR_BAD_PLAN, and every access still
 stays inside the pools and tables.  The product library sweeps when the
-records copy 64 KiB or more per page on average into a token-major
-destination; a shape with 256 KiB pages checks it there, and the full-size
-handoff is checked on every layer in test_gpu_full."""
+records copy 64 KiB or more per page on average; a shape with 256 KiB pages
+checks it there, and the full-size handoff, MLA, relayout, TP reshard and
+fork are checked on every layer in test_gpu_full."""
 import numpy as np
 import pytest
 
@@ -302,8 +302,8 @@ def test_graph_replays_of_the_product_sweep():
 @pytest.mark.parametrize("ls,ld", [("LPCTHD", "LPCTHD"), ("PLCHTD", "PLCTHD"), ("LPCTHD", "PLCHTD")])
 def test_product_library_sweeps_large_tiles(ls, ld, tokens):
     """256 KiB pages (2 kv x 64 tokens x 8 heads x 256-byte rows): the product
-    library itself takes the sweep into the token-major destinations (and
-    the persistent launch into the head-major one)."""
+    library itself takes the sweep, into token-major and head-major
+    destinations."""
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
