@@ -313,9 +313,9 @@ typedef struct kvx_plan_slot {
  * layer, layer by layer and page by page, every page on one XCD, instead of
  * a persistent grid.  Started in that order by the hardware, the pieces in
  * flight stay within a small window that slides through the transfer; on
- * MI355X this holds the handoff's 256 KiB pages at 6.1 TB/s and MLA's 72 KiB
- * pages at 5.9 TB/s in every process, where the persistent grid ranges from
- * 5.1 to 6.4 TB/s with the physical placement of the pools.
+ * MI355X this holds the handoff's 256 KiB pages at 6.1-6.35 TB/s and MLA's
+ * 72 KiB pages at 5.75-5.97 TB/s in every process, where the persistent grid
+ * ranges from 5.1 to 6.4 TB/s with the physical placement of the pools.
  * Otherwise the call runs as the unplanned one and the plan is not read.
  * Results, error bits and every rule are those of kvx_transfer(_slice):
  * - a plan that disagrees with the records, or with the pools' page sizes,
