@@ -8,7 +8,10 @@ largest workload, the MLA latent cache:
 - about 18.7k-page pools on both sides, layout [layer][page][kv][token][head][dim];
 - 64 requests with lengths uniform in [4096, 32768], copying positions
   [p, len) with p uniform in [0, len/2), so pages start unaligned.
-A step is one kvx_transfer of all 64 requests.  The same run then measures
+A step is one planned transfer (kvx_transfer_planned) of all 64 requests.
+The library picks between its two launches by timing both on the first
+warmup steps (``--launch-choice``), and ``roofline.launch`` names the one the
+timed steps took.  The same run then measures
 the other three transfer workloads of the benchmark set, one at a time
 (each allocates its pools, is timed, sample-checked against the CPU oracle
 and freed before the next), and reports them under ``context.configs``:
@@ -88,6 +91,12 @@ def traffic_record(key: str):
     return rec
 
 
+# --launch-choice values and their KVX_CHOOSE_* modes
+LAUNCH_CHOICES = {"measured": 0, "sweep": 1, "grid": 2}
+# Calls the library's measured launch choice takes on a pool pair before it
+# keeps one launch (six untimed, four timed).
+CHOICE_CALLS = 10
+
 WORKLOADS = ["mla", "handoff", "relayout", "host_tier", "tp_reshard", "cow_fork",
              "handoff_layered", "small_requests", "host_tier_v", "page_hash"]
 
@@ -96,7 +105,7 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=None, choices=WORKLOADS,
                     help="measure one workload alone (default: the MLA headline plus the "
                          "handoff, relayout and host tier under context.configs)")
@@ -109,6 +118,9 @@ def parse():
     ap.add_argument("--no-memcpy", action="store_true", help="skip the hipMemcpy reference")
     ap.add_argument("--unplanned", action="store_true",
                     help="launch transfers with kvx_transfer(_slice, _layered) instead of their planned forms")
+    ap.add_argument("--launch-choice", default="measured", choices=("measured", "sweep", "grid"),
+                    help="how planned transfers that can sweep pick their launch (kvx_set_launch_choice); "
+                         "measured, the library's default, times both on the warmup steps")
     ap.add_argument("--calibrate-copy", type=float, default=0.0, metavar="GIB",
                     help="only run a plain device copy of this many GiB (counter calibration)")
     return ap.parse_args()
@@ -149,6 +161,7 @@ def main() -> int:
         log("libkvx.so missing: building")
         build_lib.build()
     kvx.lib()
+    kvx.kvx_set_launch_choice(LAUNCH_CHOICES[args.launch_choice])
     if args.workload == "page_hash":
         return hash_bench(args)
 
@@ -266,14 +279,21 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
     steps = args.steps if not host_leg else min(args.steps, 5)
     warmup = args.warmup if not host_leg else min(args.warmup, 1)
 
-    log(f"warmup: {warmup} steps")
-    for _ in range(warmup):
+    # A planned transfer in the measured launch choice settles on one launch
+    # within CHOICE_CALLS calls; fewer warmup steps get the missing calls
+    # first, untimed, so that the timed steps all take the kept launch.
+    choosing = (kvx.kvx_launch_choice() == kvx.CHOOSE_MEASURED and
+                any(d.get("plan") is not None and not d["st"].layer_group for d in dsteps))
+    choice_calls = max(0, CHOICE_CALLS - warmup) if choosing else 0
+    log(f"warmup: {warmup} steps" + (f" after {choice_calls} launch-choice calls" if choice_calls else ""))
+    for _ in range(choice_calls + warmup):
         for d in dsteps:
             launch_step(kvx, wl, mem, d, errw)
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
     events = [[] for _ in dsteps]
+    launches = [set() for _ in dsteps]     # the launch kinds each step took while timed
     log(f"timing: {steps} steps")
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -285,6 +305,7 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
             launch_step(kvx, wl, mem, d, errw)
             e1.record(stream)
             events[i].append((e0, e1))
+            launches[i].add(kvx.LAUNCH_NAMES[kvx.kvx_last_launch()])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     dev_err = int(errw.item())
@@ -301,25 +322,29 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
     i_dom = max(range(len(dsteps)), key=lambda i: kern_ms[i])
     dom = wl.steps[i_dom]
     dom_bytes = wl.algorithmic_bytes(dom)
+    launch = "+".join(sorted(launches[i_dom]))
+    log(f"launch of the timed steps: {launch}")
     tr = traffic_record(name)
+    traffic = tr.get("by_launch", {}).get(launch) if tr else None
     if host_leg:
         one_way = dom_bytes / 2
         rate = one_way / (kern_ms[i_dom] / 1e3) / 1e9
         roofline = {"bound": "pcie", "achieved": round(rate, 2), "peak": PCIE_PEAK_GBPS,
                     "unit": "GB/s", "frac": round(rate / PCIE_PEAK_GBPS, 4),
-                    "traffic": tr["traffic_bytes_per_launch"] if tr else None,
-                    "kernel": f"kvx {dom.op}", "bytes_per_launch": int(one_way),
-                    "kernel_ms": round(kern_ms[i_dom], 4)}
+                    "traffic": traffic, "kernel": f"kvx {dom.op}", "launch": launch,
+                    "bytes_per_launch": int(one_way), "kernel_ms": round(kern_ms[i_dom], 4)}
     else:
         rate = dom_bytes / (kern_ms[i_dom] / 1e3) / 1e9
         roofline = {"bound": "hbm", "achieved": round(rate, 1), "peak": HBM_PEAK_GBPS,
                     "unit": "GB/s", "frac": round(rate / HBM_PEAK_GBPS, 4),
-                    "traffic": tr["traffic_bytes_per_launch"] if tr else None,
-                    "kernel": f"kvx {dom.op}", "bytes_per_launch": int(dom_bytes),
-                    "kernel_ms": round(kern_ms[i_dom], 4)}
+                    "traffic": traffic, "kernel": f"kvx {dom.op}", "launch": launch,
+                    "bytes_per_launch": int(dom_bytes), "kernel_ms": round(kern_ms[i_dom], 4)}
 
     reps = [sorted(a.elapsed_time(b) for a, b in ev) for ev in events]
     context = {"kernel_sha": kernel_sha(name),
+               "launch_choice": {v: k for k, v in LAUNCH_CHOICES.items()}[kvx.kvx_launch_choice()],
+               "launches": ["+".join(sorted(x)) for x in launches],
+               "launch_choice_calls": choice_calls,
                "per_step_kernel_ms": [round(x, 4) for x in kern_ms],
                "per_step_kernel_ms_median": [round(r[len(r) // 2], 4) for r in reps],
                "per_step_kernel_ms_min": [round(r[0], 4) for r in reps]}

@@ -308,14 +308,18 @@ typedef struct kvx_plan_slot {
  *   well-formed records (kvx_plan_pages returns both).  Read on the host to
  *   shape the launch.
  * When the records copy at least 64 KiB per destination page and layer on
- * average and both tables hold at most INT32_MAX entries, the library
- * launches one workgroup per 1 KiB piece of each destination page of each
+ * average and both tables hold at most INT32_MAX entries, the call can
+ * sweep: one workgroup per 1 KiB piece of each destination page of each
  * layer, layer by layer and page by page, every page on one XCD, instead of
  * a persistent grid.  Started in that order by the hardware, the pieces in
  * flight stay within a small window that slides through the transfer; on
  * MI355X this holds the handoff's 256 KiB pages at 6.1-6.35 TB/s and MLA's
  * 72 KiB pages at 5.75-5.97 TB/s in every process, where the persistent grid
- * ranges from 5.1 to 6.4 TB/s with the physical placement of the pools.
+ * ranges from 5.1 to 6.4 TB/s with the physical placement of the pools
+ * (for MLA above the sweep in most processes, 3-8% below it in others).
+ * Which of the two launches such a call takes follows
+ * kvx_set_launch_choice(): by default the faster one on these pools, found
+ * by timing both on the first calls.
  * Otherwise the call runs as the unplanned one and the plan is not read.
  * Results, error bits and every rule are those of kvx_transfer(_slice):
  * - a plan that disagrees with the records, or with the pools' page sizes,
@@ -345,6 +349,47 @@ int kvx_transfer_layered_planned(const kvx_pool *src, const kvx_pool *dst, const
                                  int32_t layers_per_group, void *const *events, int32_t n_events,
                                  const void *plan, int64_t plan_pages, int64_t plan_tokens,
                                  uint32_t *dev_err, void *stream);
+
+/* How a kvx_transfer_planned call that can sweep picks its launch.  Both
+ * launches write the same bytes; which is faster depends on where the pools
+ * sit in physical memory, and that does not change while they live.
+ * - KVX_CHOOSE_MEASURED (the default): per key (device, both pool base
+ *   pointers and descriptors, slice, n_reqs, plan_pages, plan_tokens) the
+ *   first six calls take the sweep and the persistent grid in turn,
+ *   untimed (the first calls on fresh pools run slow, whichever launch they
+ *   take); the next four are timed between HIP events, in the order sweep,
+ *   grid, grid, sweep, so that a drift that remains weighs on both launches
+ *   alike.  Once all four have completed (polled with
+ *   hipEventQuery, never waited on) every later call takes the launch with
+ *   the smaller total.  Until then calls sweep.  Calls made while their
+ *   stream is being captured record no events: they take the key's decided
+ *   launch, else the sweep, and do not count.  Eight HIP events per key in
+ *   measurement are the only resources this takes (no device memory); at
+ *   most 64 keys are kept, the least recently used dropped first.  A caller
+ *   that frees its pools and gets new ones at the same addresses keeps the
+ *   old decision until the next kvx_set_launch_choice().
+ * - KVX_CHOOSE_SWEEP: always the sweep.
+ * - KVX_CHOOSE_GRID: always the persistent grid.
+ * kvx_transfer_layered_planned sweeps every group whenever the sweep can
+ * serve it, except under KVX_CHOOSE_GRID.  The setting is process-wide;
+ * setting it (to any mode) forgets every key.  Returns KVX_OK, or
+ * KVX_ERR_RANGE for another value. */
+#define KVX_CHOOSE_MEASURED 0
+#define KVX_CHOOSE_SWEEP 1
+#define KVX_CHOOSE_GRID 2
+int kvx_set_launch_choice(int mode);
+
+/* The current KVX_CHOOSE_* mode. */
+int kvx_launch_choice(void);
+
+/* Launch kinds reported by kvx_last_launch(). */
+#define KVX_LAUNCH_NONE 0   /* the call enqueued no kernel */
+#define KVX_LAUNCH_GRID 1   /* the persistent grid */
+#define KVX_LAUNCH_SWEEP 2  /* the sweep */
+
+/* The kind of the last kernel the calling thread's last copy call
+ * (transfer, gather or scatter, any variant) enqueued. */
+int kvx_last_launch(void);
 
 /* Sizes a plan from a host copy of the records: writes the exclusive prefix
  * of pages per record into prefix[0..n_reqs] and the tokens of the

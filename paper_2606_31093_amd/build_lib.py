@@ -16,11 +16,13 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIBRARY = os.path.join(PKG, "libkvx.so")
 # The test build: its hash chain gives up after one empty poll, and planned
-# transfers of any size take the sweep launch, with at most 2048 workgroups,
-# so that larger cases loop over page slots.  These are compile-time options:
-# the product library has no switch for them.
+# transfers of any size take the sweep launch (its launch choice starts as
+# KVX_CHOOSE_SWEEP), with at most 2048 workgroups, so that larger cases loop
+# over page slots.  These are compile-time options: the product library has
+# no switch for them.
 TEST_LIBRARY = os.path.join(PKG, "libkvx_test.so")
-TEST_DEFINES = ("KVX_HASH_IDLE_POLLS=1", "KVX_SWEEP_MIN_BYTES=0", "KVX_SWEEP_MAX_BLOCKS=2048")
+TEST_DEFINES = ("KVX_HASH_IDLE_POLLS=1", "KVX_SWEEP_MIN_BYTES=0", "KVX_SWEEP_MAX_BLOCKS=2048",
+                "KVX_LAUNCH_CHOICE_DEFAULT=1")
 SOURCES = [os.path.join(CSRC, "kvx_kernels.hip"), os.path.join(CSRC, "kvx_hash.hip"),
            os.path.join(CSRC, "kvx_api.cpp")]
 HEADERS = [os.path.join(INCLUDE, "kvx.h"), os.path.join(CSRC, "kvx_internal.h"),

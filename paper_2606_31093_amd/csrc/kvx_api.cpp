@@ -1,13 +1,19 @@
 // kvx_api.cpp -- the C-ABI of libkvx (include/kvx.h): host-side validation
-// of descriptors, derivation of byte strides per layout, and the launch of
-// the copy kernel on the caller's stream.  Nothing is allocated here.
+// of descriptors, derivation of byte strides per layout, the choice between
+// the sweep and the persistent grid for planned transfers, and the launch
+// of the copy kernel on the caller's stream.  No device memory is allocated
+// here.
 
 #include <hip/hip_runtime.h>
 #include <stdarg.h>
 #include <stdio.h>
 
 #include <algorithm>
+#include <atomic>
+#include <cstring>
+#include <mutex>
 #include <string>
+#include <vector>
 
 #include "kvx.h"
 #include "kvx_hash.h"
@@ -16,6 +22,7 @@
 namespace {
 
 thread_local std::string g_last_error;
+thread_local int g_last_launch = KVX_LAUNCH_NONE;
 
 int fail(int status, const char *fmt, ...) {
     char msg[512];
@@ -303,6 +310,7 @@ int enqueue(const kvx::Params &P, void *stream) {
     int e = kvx::launch(P, static_cast<hipStream_t>(stream));
     if (e != hipSuccess)
         return fail(KVX_ERR_HIP, "kernel launch failed: %s", hipGetErrorString((hipError_t)e));
+    g_last_launch = P.sweep ? KVX_LAUNCH_SWEEP : KVX_LAUNCH_GRID;
     return KVX_OK;
 }
 
@@ -368,12 +376,140 @@ void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t pl
     P.fd_hv = kvx::make_fastdiv((uint32_t)(P.H * P.vpr));
 }
 
+#ifndef KVX_LAUNCH_CHOICE_DEFAULT
+#define KVX_LAUNCH_CHOICE_DEFAULT KVX_CHOOSE_MEASURED
+#endif
+
+// Launch choice of a planned single-launch transfer that can sweep (the
+// rules are in include/kvx.h, kvx_set_launch_choice).  Both launches write
+// the same bytes.  Which one is faster depends on where the pools sit in
+// physical memory: for MLA's 72 KiB pages the persistent grid ran 1-8%
+// above the sweep in most fresh processes and 3-9% below it in the rest,
+// while each process's own rate held within 0.3% once warm.  So the first
+// calls of a key run each launch once, then time each once, and later calls
+// keep the faster.
+struct TuneKey {
+    int dev;
+    const void *src, *dst;
+    kvx_pool sp, dp;
+    kvx_slice sl;
+    int32_t n_reqs;
+    int64_t plan_pages, plan_tokens;
+};
+
+// After six untimed calls (the launches in turn), four timed calls in the
+// order sweep, grid, grid, sweep.  The first calls on fresh pools run slow
+// (the first by up to 30%, and short ones for a few milliseconds more, the
+// sweep longer than the grid); the order of the timed calls makes a drift
+// that remains weigh on both sums alike.
+constexpr int kUntimed = 6;
+constexpr int kTimed = 4;
+constexpr int kTimedLaunch[kTimed] = {KVX_LAUNCH_SWEEP, KVX_LAUNCH_GRID, KVX_LAUNCH_GRID,
+                                      KVX_LAUNCH_SWEEP};
+
+struct Tune {
+    TuneKey key;
+    int calls;                 // calls seen before the decision
+    int choice;                // KVX_LAUNCH_SWEEP or KVX_LAUNCH_GRID once decided, else 0
+    hipEvent_t ev[2 * kTimed]; // start and end of each timed call
+    uint64_t used;             // recency, for dropping the least recently used key
+};
+
+constexpr size_t kMaxTunes = 64;
+std::mutex g_tune_mu;
+std::vector<Tune> g_tunes;   // never destroyed: events are not released at exit
+uint64_t g_tune_clock = 0;
+std::atomic<int> g_choice_mode{KVX_LAUNCH_CHOICE_DEFAULT};
+
+void drop_events(Tune &t) {
+    for (hipEvent_t &e : t.ev)
+        if (e) {
+            (void)hipEventDestroy(e);
+            e = nullptr;
+        }
+}
+
+// Decides t once every timed call has completed; false while one is pending.
+bool decide(Tune &t) {
+    float sum[3] = {0.f, 0.f, 0.f};   // by launch kind
+    bool ok = true;
+    for (int k = 0; k < kTimed && ok; ++k) {
+        const hipError_t q = hipEventQuery(t.ev[2 * k + 1]);
+        if (q == hipErrorNotReady) return false;
+        float ms = 0.f;
+        ok = q == hipSuccess && hipEventElapsedTime(&ms, t.ev[2 * k], t.ev[2 * k + 1]) == hipSuccess;
+        sum[kTimedLaunch[k]] += ms;
+    }
+    t.choice = ok && sum[KVX_LAUNCH_GRID] < sum[KVX_LAUNCH_SWEEP] ? KVX_LAUNCH_GRID : KVX_LAUNCH_SWEEP;
+    drop_events(t);
+    return true;
+}
+
+// The launch for this call (KVX_LAUNCH_SWEEP or KVX_LAUNCH_GRID) and, when
+// the call is timed, the events to record around it (else null).
+int pick_launch(const TuneKey &key, hipStream_t stream, hipEvent_t *t0, hipEvent_t *t1) {
+    *t0 = *t1 = nullptr;
+    std::lock_guard<std::mutex> lock(g_tune_mu);
+    if (g_choice_mode == KVX_CHOOSE_SWEEP) return KVX_LAUNCH_SWEEP;
+    if (g_choice_mode == KVX_CHOOSE_GRID) return KVX_LAUNCH_GRID;
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    const bool capturing = hipStreamIsCapturing(stream, &cs) != hipSuccess ||
+                           cs != hipStreamCaptureStatusNone;
+    Tune *t = nullptr;
+    for (Tune &x : g_tunes)
+        if (std::memcmp(&x.key, &key, sizeof key) == 0) t = &x;
+    if (!t) {
+        if (capturing) return KVX_LAUNCH_SWEEP;
+        if (g_tunes.size() == kMaxTunes) {
+            auto old = std::min_element(g_tunes.begin(), g_tunes.end(),
+                                        [](const Tune &a, const Tune &b) { return a.used < b.used; });
+            drop_events(*old);
+            g_tunes.erase(old);
+        }
+        g_tunes.push_back(Tune{});
+        t = &g_tunes.back();
+        std::memcpy(&t->key, &key, sizeof key);   // padding included: keys compare with memcmp
+    }
+    t->used = ++g_tune_clock;
+    if (t->choice) return t->choice;
+    if (capturing) return KVX_LAUNCH_SWEEP;
+    const int k = t->calls - kUntimed;          // index of this call among the timed ones
+    if (k >= kTimed) return decide(*t) ? t->choice : KVX_LAUNCH_SWEEP;
+    ++t->calls;
+    if (k < 0) return (k + kUntimed) % 2 ? KVX_LAUNCH_GRID : KVX_LAUNCH_SWEEP;   // untimed
+    if (k == 0)
+        for (hipEvent_t &e : t->ev)
+            if (hipEventCreate(&e) != hipSuccess) {
+                e = nullptr;
+                drop_events(*t);
+                t->choice = KVX_LAUNCH_SWEEP;
+                return t->choice;
+            }
+    *t0 = t->ev[2 * k];
+    *t1 = t->ev[2 * k + 1];
+    return kTimedLaunch[k];
+}
+
+// Enqueue P (one launch of a transfer that plan_sweep may have set to sweep)
+// with the launch pick_launch gives, timed when it says so.
+int enqueue_chosen(kvx::Params &P, const TuneKey &key, void *stream) {
+    if (!P.sweep) return enqueue(P, stream);
+    const hipStream_t hs = static_cast<hipStream_t>(stream);
+    hipEvent_t t0, t1;
+    P.sweep = pick_launch(key, hs, &t0, &t1) == KVX_LAUNCH_SWEEP;
+    if (t0 && hipEventRecord(t0, hs) != hipSuccess) t0 = t1 = nullptr;
+    const int st = enqueue(P, stream);
+    if (st == KVX_OK && t1) (void)hipEventRecord(t1, hs);
+    return st;
+}
+
 int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *slice,
                   const int32_t *src_pt, int64_t src_pt_len, const int32_t *dst_pt,
                   int64_t dst_pt_len, const kvx_req *reqs, int32_t n_reqs, uint32_t *dev_err,
                   void *stream, int32_t group = 0, void *const *events = nullptr,
                   int32_t n_events = 0, const void *plan = nullptr, int64_t plan_pages = -1,
                   int64_t plan_tokens = -1) {
+    g_last_launch = KVX_LAUNCH_NONE;
     Shape ss, ds;
     int st;
     if ((st = check_pool(src, "src", ss))) return st;
@@ -422,7 +558,24 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
                               sl.dst_head0, sl.num_heads);
             finish_params(P, Shape{nl, sl.num_kv, sl.num_heads, ss.D, ss.e}, v, n_reqs);
             plan_sweep(P, plan, plan_pages, plan_tokens);
-            if ((st = enqueue(P, stream))) return st;
+            if (group > 0) {
+                if (g_choice_mode == KVX_CHOOSE_GRID) P.sweep = 0;
+                st = enqueue(P, stream);
+            } else {
+                TuneKey key;
+                std::memset(&key, 0, sizeof key);
+                if (hipGetDevice(&key.dev) != hipSuccess) key.dev = -1;
+                key.src = src->base;
+                key.dst = dst->base;
+                key.sp = *src;
+                key.dp = *dst;
+                key.sl = sl;
+                key.n_reqs = n_reqs;
+                key.plan_pages = plan_pages;
+                key.plan_tokens = plan_tokens;
+                st = enqueue_chosen(P, key, stream);
+            }
+            if (st) return st;
         }
         if (group > 0) {
             const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(events[g]), hs);
@@ -470,6 +623,7 @@ int check_buffer_slice(const kvx_slice &sl, const Shape &pool, const Shape &buf,
 int buffer_impl(int op, const kvx_pool *pool, const kvx_buf *buf, const kvx_slice *slice,
                 const int32_t *pt, int64_t pt_len, const kvx_req *reqs, int32_t n_reqs,
                 uint32_t *dev_err, void *stream) {
+    g_last_launch = KVX_LAUNCH_NONE;
     const bool gather = op == kvx::OP_GATHER;
     const char *pname = gather ? "src" : "dst", *bname = gather ? "dst" : "src";
     const char *tname = gather ? "src_pt" : "dst_pt";
@@ -751,6 +905,21 @@ const char *kvx_strerror(int status) {
 }
 
 const char *kvx_last_error(void) { return g_last_error.c_str(); }
+
+int kvx_set_launch_choice(int mode) {
+    g_last_error.clear();
+    if (mode != KVX_CHOOSE_MEASURED && mode != KVX_CHOOSE_SWEEP && mode != KVX_CHOOSE_GRID)
+        return fail(KVX_ERR_RANGE, "launch choice %d is not a KVX_CHOOSE_* mode", mode);
+    std::lock_guard<std::mutex> lock(g_tune_mu);
+    for (Tune &t : g_tunes) drop_events(t);
+    g_tunes.clear();
+    g_choice_mode = mode;
+    return KVX_OK;
+}
+
+int kvx_launch_choice(void) { return g_choice_mode.load(); }
+
+int kvx_last_launch(void) { return g_last_launch; }
 
 int kvx_abi_version(void) { return KVX_ABI_VERSION; }
 

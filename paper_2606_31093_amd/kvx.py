@@ -146,6 +146,12 @@ def load(path: str) -> ctypes.CDLL:
     L.kvx_last_error.restype = ctypes.c_char_p
     L.kvx_abi_version.argtypes = []
     L.kvx_abi_version.restype = ctypes.c_int
+    L.kvx_set_launch_choice.argtypes = [ctypes.c_int]
+    L.kvx_set_launch_choice.restype = ctypes.c_int
+    L.kvx_launch_choice.argtypes = []
+    L.kvx_launch_choice.restype = ctypes.c_int
+    L.kvx_last_launch.argtypes = []
+    L.kvx_last_launch.restype = ctypes.c_int
     return L
 
 
@@ -533,3 +539,28 @@ def kvx_last_error() -> str:
 
 def kvx_abi_version() -> int:
     return int(lib().kvx_abi_version())
+
+
+# Launch choice of planned transfers and launch kinds (include/kvx.h).
+CHOOSE_MEASURED, CHOOSE_SWEEP, CHOOSE_GRID = 0, 1, 2
+LAUNCH_NONE, LAUNCH_GRID, LAUNCH_SWEEP = 0, 1, 2
+LAUNCH_NAMES = {LAUNCH_NONE: "none", LAUNCH_GRID: "grid", LAUNCH_SWEEP: "sweep"}
+
+
+def kvx_set_launch_choice(mode: int, library=None) -> None:
+    """How planned transfers that can sweep pick their launch: CHOOSE_MEASURED,
+    CHOOSE_SWEEP or CHOOSE_GRID (process-wide; forgets earlier measurements)."""
+    L = library or lib()
+    status = L.kvx_set_launch_choice(int(mode))
+    if status != 0:
+        raise KvxError(status, L.kvx_last_error().decode())
+
+
+def kvx_launch_choice(library=None) -> int:
+    return int((library or lib()).kvx_launch_choice())
+
+
+def kvx_last_launch(library=None) -> int:
+    """LAUNCH_NONE, LAUNCH_GRID or LAUNCH_SWEEP: the kind of the last kernel
+    this thread's last copy call enqueued."""
+    return int((library or lib()).kvx_last_launch())

@@ -572,3 +572,46 @@ def test_test_build_exports_the_same_functions():
     out = subprocess.run(["nm", "-D", "--defined-only", build_lib.TEST_LIBRARY], capture_output=True,
                          text=True, check=True).stdout
     assert set(declared_functions()) <= set(re.findall(r"\b(kvx_\w+)$", out, flags=re.M))
+
+
+def _header_defines(prefix):
+    text = open(HEADER).read()
+    return {m.group(1): int(m.group(2)) for m in re.finditer(rf"#define ({prefix}\w+) (-?\d+)", text)}
+
+
+def test_launch_constants_match_the_header():
+    choose, launch = _header_defines("KVX_CHOOSE_"), _header_defines("KVX_LAUNCH_")
+    assert choose == {"KVX_CHOOSE_MEASURED": kvx.CHOOSE_MEASURED, "KVX_CHOOSE_SWEEP": kvx.CHOOSE_SWEEP,
+                      "KVX_CHOOSE_GRID": kvx.CHOOSE_GRID}
+    assert launch == {"KVX_LAUNCH_NONE": kvx.LAUNCH_NONE, "KVX_LAUNCH_GRID": kvx.LAUNCH_GRID,
+                      "KVX_LAUNCH_SWEEP": kvx.LAUNCH_SWEEP}
+
+
+def test_launch_choice_modes(lib):
+    """The product library measures by default; every mode can be set, and
+    anything else is refused without changing the mode."""
+    assert kvx.kvx_launch_choice() == kvx.CHOOSE_MEASURED
+    try:
+        for mode in (kvx.CHOOSE_SWEEP, kvx.CHOOSE_GRID, kvx.CHOOSE_MEASURED):
+            kvx.kvx_set_launch_choice(mode)
+            assert kvx.kvx_launch_choice() == mode
+        for bad in (-1, 3, 1 << 20):
+            with pytest.raises(kvx.KvxError) as e:
+                kvx.kvx_set_launch_choice(bad)
+            assert e.value.status == -5 and "KVX_CHOOSE" in str(e.value)
+            assert kvx.kvx_launch_choice() == kvx.CHOOSE_MEASURED
+    finally:
+        kvx.kvx_set_launch_choice(kvx.CHOOSE_MEASURED)
+
+
+def test_test_build_starts_sweeping():
+    test_lib = kvx.load(build_lib.TEST_LIBRARY)
+    assert kvx.kvx_launch_choice(test_lib) == kvx.CHOOSE_SWEEP
+
+
+def test_refused_call_reports_no_launch(lib):
+    spec = PoolSpec(2, 2, 2, 64, T=16, N=4)
+    pool = kvx.pool_desc(spec)
+    status = lib.kvx_transfer(ctypes.byref(pool), None, None, 0, None, 0, None, 0, None, None)
+    assert status == -1
+    assert kvx.kvx_last_launch() == kvx.LAUNCH_NONE
