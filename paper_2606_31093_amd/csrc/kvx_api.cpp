@@ -446,10 +446,10 @@ bool decide(Tune &t) {
 }
 
 // The launch for this call (KVX_LAUNCH_SWEEP or KVX_LAUNCH_GRID) and, when
-// the call is timed, the events to record around it (else null).
+// the call is timed, the events to record around it (else null).  Called
+// with g_tune_mu held.
 int pick_launch(const TuneKey &key, hipStream_t stream, hipEvent_t *t0, hipEvent_t *t1) {
     *t0 = *t1 = nullptr;
-    std::lock_guard<std::mutex> lock(g_tune_mu);
     if (g_choice_mode == KVX_CHOOSE_SWEEP) return KVX_LAUNCH_SWEEP;
     if (g_choice_mode == KVX_CHOOSE_GRID) return KVX_LAUNCH_GRID;
     hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
@@ -491,13 +491,20 @@ int pick_launch(const TuneKey &key, hipStream_t stream, hipEvent_t *t0, hipEvent
 }
 
 // Enqueue P (one launch of a transfer that plan_sweep may have set to sweep)
-// with the launch pick_launch gives, timed when it says so.
+// with the launch pick_launch gives.  A timed call records its events and
+// launches with the lock still held, so that no other call of the key
+// queries or destroys the events before they are recorded.
 int enqueue_chosen(kvx::Params &P, const TuneKey &key, void *stream) {
     if (!P.sweep) return enqueue(P, stream);
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     hipEvent_t t0, t1;
+    std::unique_lock<std::mutex> lock(g_tune_mu);
     P.sweep = pick_launch(key, hs, &t0, &t1) == KVX_LAUNCH_SWEEP;
-    if (t0 && hipEventRecord(t0, hs) != hipSuccess) t0 = t1 = nullptr;
+    if (!t0) {
+        lock.unlock();
+        return enqueue(P, stream);
+    }
+    if (hipEventRecord(t0, hs) != hipSuccess) t1 = nullptr;
     const int st = enqueue(P, stream);
     if (st == KVX_OK && t1) (void)hipEventRecord(t1, hs);
     return st;

@@ -165,3 +165,42 @@ def test_captured_call_records_nothing_and_replays_exact(kvx):
     assert [c.call() for _ in range(9)] == MEASURE[1:]       # the measurement goes on
     torch.cuda.synchronize()
     assert c.call() in (S, G)
+
+
+def test_two_threads_measure_one_key(kvx):
+    """Two host threads on two streams make the calls of one key while it is
+    measured (both write the same bytes into the same pools).  Every call
+    returns, the result is the oracle's, and afterwards the key keeps one
+    launch."""
+    import threading
+
+    import torch
+    c = Case(kvx, seed=57)
+    S, G = kvx.LAUNCH_SWEEP, kvx.LAUNCH_GRID
+    c.b.copy_(c.b0)
+    torch.cuda.synchronize()
+    failures = []
+
+    def worker():
+        s = torch.cuda.Stream()
+        try:
+            with torch.cuda.stream(s):
+                for _ in range(12):
+                    kvx.kvx_transfer_planned(c.a, c.S, c.b, c.D, c.spt, c.dpt, c.reqs, c.plan, c.pages,
+                                             c.tokens, None, c.err, stream=s)
+            s.synchronize()
+        except Exception as e:           # reported below, on the test's thread
+            failures.append(e)
+
+    threads = [threading.Thread(target=worker) for _ in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not failures, failures
+    assert int(c.err.item()) == 0
+    assert np.array_equal(c.b.cpu().numpy(), c.want)
+    decided = c.call()
+    assert decided in (S, G)
+    assert [c.call() for _ in range(3)] == [decided] * 3
