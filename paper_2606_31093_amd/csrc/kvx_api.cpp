@@ -386,8 +386,8 @@ void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t pl
 // physical memory: for MLA's 72 KiB pages the persistent grid ran 1-8%
 // above the sweep in most fresh processes and 3-9% below it in the rest,
 // while each process's own rate held within 0.3% once warm.  So the first
-// calls of a key run each launch once, then time each once, and later calls
-// keep the faster.
+// calls of a key warm both launches, then time both, and later calls keep
+// the faster.
 struct TuneKey {
     int dev;
     const void *src, *dst;
