@@ -349,14 +349,16 @@ void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t pl
     P.sweep = 0;
     if (!plan || plan_pages < 1 || plan_tokens < 1 || P.n_reqs < 1 || P.op != kvx::OP_TRANSFER) return;
     if (P.src.pt_len > INT32_MAX || P.dst.pt_len > INT32_MAX) return;
-    const int64_t T = P.dst.T, rows_per_head =
-        P.dst.tok_contig ? T : (T + KVX_SLOT_BLOCK - 1) / KVX_SLOT_BLOCK * KVX_SLOT_BLOCK + KVX_SLOT_BLOCK;
+    // rows per head of a page's enumeration: a head-major destination takes
+    // whole blocks of slots, aligned to the page, so any slot range of a page
+    // covers at most its ceil(T / block) blocks
+    constexpr int64_t SB = KVX_SWEEP_SLOT_BLOCK;
+    const int64_t T = P.dst.T, rows_per_head = P.dst.tok_contig ? T : (T + SB - 1) / SB * SB;
     // average bytes copied per destination page and layer
     const int64_t token_bytes = (int64_t)P.C * P.H * P.row_bytes;
     if (plan_tokens > INT64_MAX / token_bytes || plan_tokens * token_bytes < KVX_SWEEP_MIN_BYTES * plan_pages)
         return;
-    // pieces of 64 vectors per page: the vectors of the page's enumeration (a
-    // head-major destination covers whole slot blocks, a few slots more)
+    // pieces of 64 vectors per page: the vectors of the page's enumeration
     const int64_t tile_vecs = (int64_t)P.C * rows_per_head * P.H * P.vpr;
     // workgroups per page: KVX_SWEEP_PIECES pieces each
     const int64_t ppt = ((tile_vecs + 63) / 64 + KVX_SWEEP_PIECES - 1) / KVX_SWEEP_PIECES;

@@ -453,14 +453,15 @@ __global__ void __launch_bounds__(kBlock) kvx_copy_kernel(Params p) {
     }
 }
 
-// Lane k's row of a tile in the vector order of copy_rows: kv component c,
-// slot, head h, vector v of the row; valid is cleared for a masked slot of a
-// head-major tiling side.
+// Lane k's row of a sweep piece: kv component c, slot, head h, vector v of
+// the row, in the vector order of copy_rows (a head-major destination in
+// blocks of KVX_SWEEP_SLOT_BLOCK slots); valid is cleared for a masked slot
+// of a head-major destination.
 template <bool TTHD>
 __device__ __forceinline__ void tile_row(const Params &p, uint32_t k, uint32_t rows_c, int32_t sa,
                                          int32_t sb, uint32_t blk0, uint32_t &c, uint32_t &slot,
                                          uint32_t &h, uint32_t &v, bool &valid) {
-    constexpr uint32_t SB = KVX_SLOT_BLOCK;
+    constexpr uint32_t SB = KVX_SWEEP_SLOT_BLOCK;
     const uint32_t rw = fd_div(p.fd_vpr, k);
     v = k - rw * p.vpr;
     c = rw >= rows_c;
@@ -480,8 +481,8 @@ __device__ __forceinline__ void tile_row(const Params &p, uint32_t k, uint32_t r
 
 // One piece of the sweep: the vectors [kb, kb + 64) of destination page slot
 // d of layer l, one vector per lane, in the vector order of copy_rows (a
-// head-major destination in blocks of slots, the slots outside the page's
-// range masked).  Every load of metadata on the path that copies (the slot,
+// head-major destination in blocks of KVX_SWEEP_SLOT_BLOCK slots, the slots
+// outside the page's range masked).  Every load of metadata on the path that copies (the slot,
 // the destination page id, and the source page id when all the piece's rows
 // lie in one source page, the usual case) is uniform and comes before the
 // first store or atomic, so it goes through the scalar cache.  FLAT (both
@@ -502,7 +503,7 @@ __device__ __forceinline__ void sweep_piece(const Params &p, const kvx_plan_slot
           (uint32_t)so_a < (uint32_t)os.T))
         return;
     const int32_t sb = sa + (int32_t)ntok;
-    constexpr uint32_t SB = KVX_SLOT_BLOCK;
+    constexpr uint32_t SB = KVX_SWEEP_SLOT_BLOCK;
     const uint32_t blk0 = (uint32_t)sa / SB, nblk = ((uint32_t)sb - 1) / SB - blk0 + 1;
     const uint32_t rows_c = TTHD ? ntok * p.H : p.H * nblk * SB;
     const uint32_t total = rows_c * p.vpr * (uint32_t)p.C;
