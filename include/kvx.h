@@ -359,9 +359,9 @@ int kvx_transfer_layered_planned(const kvx_pool *src, const kvx_pool *dst, const
  *   untimed (the first calls on fresh pools run slow, whichever launch they
  *   take); the next four are timed between HIP events, in the order sweep,
  *   grid, grid, sweep, so that a drift that remains weighs on both launches
- *   alike.  Once all four have completed (polled with
- *   hipEventQuery, never waited on) every later call takes the launch with
- *   the smaller total.  Until then calls sweep.  Calls made while their
+ *   alike.  Once all four have completed (polled with hipEventQuery, never
+ *   waited on) every later call takes the launch with the smaller total.
+ *   Until then calls sweep.  Calls made while their
  *   stream is being captured record no events: they take the key's decided
  *   launch, else the sweep, and do not count.  Eight HIP events per key in
  *   measurement are the only resources this takes (no device memory); at
