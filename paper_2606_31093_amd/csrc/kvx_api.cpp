@@ -364,8 +364,11 @@ void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t pl
     const int64_t ppt = ((tile_vecs + 63) / 64 + KVX_SWEEP_PIECES - 1) / KVX_SWEEP_PIECES;
     const int64_t per_slot = (int64_t)P.L * ppt;         // workgroups per page slot
     if (per_slot > KVX_SWEEP_MAX_BLOCKS) return;
-    // page slots per pass: the plan's pages in KVX_SWEEP_PASSES passes, within the grid cap
-    const int64_t want = (plan_pages + KVX_SWEEP_PASSES - 1) / KVX_SWEEP_PASSES;
+    // page slots per pass: the plan's pages in KVX_SWEEP_PASSES passes (fewer
+    // for small pages), within the grid cap
+    const int64_t passes = plan_tokens * token_bytes < KVX_SWEEP_SMALL_BYTES * plan_pages
+                               ? KVX_SWEEP_PASSES_SMALL : KVX_SWEEP_PASSES;
+    const int64_t want = (plan_pages + passes - 1) / passes;
     const int64_t slots = want < KVX_SWEEP_MAX_BLOCKS / per_slot ? want : KVX_SWEEP_MAX_BLOCKS / per_slot;
     P.sweep = 1;
     P.prefix = static_cast<const int64_t *>(plan);

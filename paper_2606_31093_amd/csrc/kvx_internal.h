@@ -28,10 +28,18 @@
 #define KVX_SWEEP_PIECES 1
 #endif
 // Passes of a sweep launch over the plan's pages: each workgroup copies its
-// piece of one page in each pass, pages plan_pages / passes apart (measured:
-// 3 passes move 128-256 KiB pages 4-6% faster than 1, 72 KiB pages within 1%).
+// piece of one page in each pass, pages plan_pages / passes apart.  Measured:
+// 3 passes move 128-256 KiB pages 4-6% faster than 1; below 128 KiB copied
+// per page and layer on average, 2 passes beat 3 by 0.5-1.5% at every page
+// size tried (64-108 KiB), where at 128 KiB and up they vary from -4% to +1%.
 #ifndef KVX_SWEEP_PASSES
 #define KVX_SWEEP_PASSES 3
+#endif
+#ifndef KVX_SWEEP_SMALL_BYTES
+#define KVX_SWEEP_SMALL_BYTES (128 << 10)
+#endif
+#ifndef KVX_SWEEP_PASSES_SMALL
+#define KVX_SWEEP_PASSES_SMALL 2
 #endif
 // Most workgroups of one sweep launch: the work-items of a launch (64 per
 // workgroup) must stay below 2^32, and this keeps them below 2^31.  Beyond
