@@ -5,7 +5,8 @@ of a key take the sweep and the persistent grid in turn, the next four
 are in, every later call takes one launch, the same each time; a new key,
 or setting the mode again, starts over.  The fixed modes always take their
 launch, a call captured in a HIP graph records no events and takes the
-sweep, and every call's result is the oracle's, bit for bit."""
+sweep, two host threads can measure one key at once, and every call's
+result is the oracle's, bit for bit."""
 import numpy as np
 import pytest
 
