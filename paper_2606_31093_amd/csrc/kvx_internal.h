@@ -29,14 +29,15 @@
 #endif
 // Passes of a sweep launch over the plan's pages: each workgroup copies its
 // piece of one page in each pass, pages plan_pages / passes apart.  Measured:
-// 3 passes move 128-256 KiB pages 4-6% faster than 1; below 128 KiB copied
-// per page and layer on average, 2 passes beat 3 by 0.5-1.5% at every page
-// size tried (64-108 KiB), where at 128 KiB and up they vary from -4% to +1%.
+// 3 passes move 128-256 KiB pages 4-6% faster than 1; 2 passes beat 3 by
+// 0.5-1.5% at every page size tried from 64 to 108 KiB, where from 121 KiB
+// copied per page and layer on average up they vary from -4% to +1%.  So
+// below 96 KiB on average a launch takes 2.
 #ifndef KVX_SWEEP_PASSES
 #define KVX_SWEEP_PASSES 3
 #endif
 #ifndef KVX_SWEEP_SMALL_BYTES
-#define KVX_SWEEP_SMALL_BYTES (128 << 10)
+#define KVX_SWEEP_SMALL_BYTES (96 << 10)
 #endif
 #ifndef KVX_SWEEP_PASSES_SMALL
 #define KVX_SWEEP_PASSES_SMALL 2
