@@ -354,14 +354,16 @@ int kvx_transfer_layered_planned(const kvx_pool *src, const kvx_pool *dst, const
  * launches write the same bytes; which is faster depends on where the pools
  * sit in physical memory, and that does not change while they live.
  * - KVX_CHOOSE_MEASURED (the default): per key (device, both pool base
- *   pointers and descriptors, slice, n_reqs, plan_pages, plan_tokens) the
- *   first six calls take the sweep and the persistent grid in turn,
+ *   pointers and descriptors, and the slice: the pair of pools, whatever
+ *   the records of each call) the first six calls take the sweep and the
+ *   persistent grid in turn,
  *   untimed (the first calls on fresh pools run slow, whichever launch they
  *   take); the next four are timed between HIP events, in the order sweep,
  *   grid, grid, sweep, so that a drift that remains weighs on both launches
  *   alike.  Once all four have completed (polled with hipEventQuery, never
- *   waited on) every later call takes the launch with the smaller total.
- *   Until then calls sweep.  Calls made while their
+ *   waited on) every later call takes the launch that moved more tokens
+ *   (plan_tokens) per millisecond over its two timed calls.  Until then
+ *   calls sweep.  Calls made while their
  *   stream is being captured record no events: they take the key's decided
  *   launch, else the sweep, and do not count.  Eight HIP events per key in
  *   measurement are the only resources this takes (no device memory); at

@@ -391,15 +391,14 @@ void plan_sweep(kvx::Params &P, const void *plan, int64_t plan_pages, int64_t pl
 // physical memory: for MLA's 72 KiB pages the persistent grid ran 1-8%
 // above the sweep in most fresh processes and 3-9% below it in the rest,
 // while each process's own rate held within 0.3% once warm.  So the first
-// calls of a key warm both launches, then time both, and later calls keep
-// the faster.
+// calls on a pair of pools warm both launches, then time both, and later
+// calls keep the faster.  The key is the pair of pools (and the slice), not
+// the records: a serving loop moves other requests in every call.
 struct TuneKey {
     int dev;
     const void *src, *dst;
     kvx_pool sp, dp;
     kvx_slice sl;
-    int32_t n_reqs;
-    int64_t plan_pages, plan_tokens;
 };
 
 // After six untimed calls (the launches in turn), four timed calls in the
@@ -417,6 +416,7 @@ struct Tune {
     int calls;                 // calls seen before the decision
     int choice;                // KVX_LAUNCH_SWEEP or KVX_LAUNCH_GRID once decided, else 0
     hipEvent_t ev[2 * kTimed]; // start and end of each timed call
+    int64_t tokens[kTimed];    // tokens each timed call moved (calls may move different amounts)
     uint64_t used;             // recency, for dropping the least recently used key
 };
 
@@ -434,26 +434,34 @@ void drop_events(Tune &t) {
         }
 }
 
-// Decides t once every timed call has completed; false while one is pending.
+// Decides t once every timed call has completed (false while one is
+// pending): the launch that moved more tokens per millisecond over its two
+// timed calls.
 bool decide(Tune &t) {
-    float sum[3] = {0.f, 0.f, 0.f};   // by launch kind
+    double ms_sum[3] = {0.0, 0.0, 0.0}, tok_sum[3] = {0.0, 0.0, 0.0};   // by launch kind
     bool ok = true;
     for (int k = 0; k < kTimed && ok; ++k) {
         const hipError_t q = hipEventQuery(t.ev[2 * k + 1]);
         if (q == hipErrorNotReady) return false;
         float ms = 0.f;
-        ok = q == hipSuccess && hipEventElapsedTime(&ms, t.ev[2 * k], t.ev[2 * k + 1]) == hipSuccess;
-        sum[kTimedLaunch[k]] += ms;
+        ok = q == hipSuccess && hipEventElapsedTime(&ms, t.ev[2 * k], t.ev[2 * k + 1]) == hipSuccess &&
+             ms > 0.f;
+        ms_sum[kTimedLaunch[k]] += ms;
+        tok_sum[kTimedLaunch[k]] += (double)t.tokens[k];
     }
-    t.choice = ok && sum[KVX_LAUNCH_GRID] < sum[KVX_LAUNCH_SWEEP] ? KVX_LAUNCH_GRID : KVX_LAUNCH_SWEEP;
+    // grid faster: tok_g / ms_g > tok_s / ms_s
+    t.choice = ok && tok_sum[KVX_LAUNCH_GRID] * ms_sum[KVX_LAUNCH_SWEEP] >
+                         tok_sum[KVX_LAUNCH_SWEEP] * ms_sum[KVX_LAUNCH_GRID]
+                   ? KVX_LAUNCH_GRID : KVX_LAUNCH_SWEEP;
     drop_events(t);
     return true;
 }
 
 // The launch for this call (KVX_LAUNCH_SWEEP or KVX_LAUNCH_GRID) and, when
-// the call is timed, the events to record around it (else null).  Called
-// with g_tune_mu held.
-int pick_launch(const TuneKey &key, hipStream_t stream, hipEvent_t *t0, hipEvent_t *t1) {
+// the call is timed, the events to record around it (else null); tokens is
+// what the call moves.  Called with g_tune_mu held.
+int pick_launch(const TuneKey &key, int64_t tokens, hipStream_t stream, hipEvent_t *t0,
+                hipEvent_t *t1) {
     *t0 = *t1 = nullptr;
     if (g_choice_mode == KVX_CHOOSE_SWEEP) return KVX_LAUNCH_SWEEP;
     if (g_choice_mode == KVX_CHOOSE_GRID) return KVX_LAUNCH_GRID;
@@ -492,6 +500,7 @@ int pick_launch(const TuneKey &key, hipStream_t stream, hipEvent_t *t0, hipEvent
             }
     *t0 = t->ev[2 * k];
     *t1 = t->ev[2 * k + 1];
+    t->tokens[k] = tokens;
     return kTimedLaunch[k];
 }
 
@@ -499,12 +508,12 @@ int pick_launch(const TuneKey &key, hipStream_t stream, hipEvent_t *t0, hipEvent
 // with the launch pick_launch gives.  A timed call records its events and
 // launches with the lock still held, so that no other call of the key
 // queries or destroys the events before they are recorded.
-int enqueue_chosen(kvx::Params &P, const TuneKey &key, void *stream) {
+int enqueue_chosen(kvx::Params &P, const TuneKey &key, int64_t tokens, void *stream) {
     if (!P.sweep) return enqueue(P, stream);
     const hipStream_t hs = static_cast<hipStream_t>(stream);
     hipEvent_t t0, t1;
     std::unique_lock<std::mutex> lock(g_tune_mu);
-    P.sweep = pick_launch(key, hs, &t0, &t1) == KVX_LAUNCH_SWEEP;
+    P.sweep = pick_launch(key, tokens, hs, &t0, &t1) == KVX_LAUNCH_SWEEP;
     if (!t0) {
         lock.unlock();
         return enqueue(P, stream);
@@ -582,10 +591,7 @@ int transfer_impl(const kvx_pool *src, const kvx_pool *dst, const kvx_slice *sli
                 key.sp = *src;
                 key.dp = *dst;
                 key.sl = sl;
-                key.n_reqs = n_reqs;
-                key.plan_pages = plan_pages;
-                key.plan_tokens = plan_tokens;
-                st = enqueue_chosen(P, key, stream);
+                st = enqueue_chosen(P, key, plan_tokens, stream);
             }
             if (st) return st;
         }

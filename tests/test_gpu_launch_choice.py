@@ -3,7 +3,8 @@ GPU through the product library.  In the measured mode the first six calls
 of a key take the sweep and the persistent grid in turn, the next four
 (timed) the sweep, the grid, the grid and the sweep, and once their timings
 are in, every later call takes one launch, the same each time; a new key,
-or setting the mode again, starts over.  The fixed modes always take their
+or setting the mode again, starts over; other records on the same pools
+share the pools' measurement.  The fixed modes always take their
 launch, a call captured in a HIP graph records no events and takes the
 sweep, two host threads can measure one key at once, and every call's
 result is the oracle's, bit for bit."""
@@ -52,20 +53,36 @@ class Case:
         self.reqs = kvx.device_reqs(self.st.reqs)
         self.plan, self.pages, self.tokens = kvx.device_plan(self.st.reqs, self.S.T, self.D.T)
         self.err = torch.zeros(1, dtype=torch.int32, device="cuda")
+        self.wl, self.init = wl, init
+        self.subset = None
+
+    def use_records(self, rows):
+        """Later calls move only these records (rows of the case's own),
+        over the same pools and tables."""
+        import dataclasses
+        if rows is None:
+            self.subset = None
+            return
+        st = dataclasses.replace(self.st, reqs=np.asarray(rows, np.int64).reshape(-1, 6))
+        wl = dataclasses.replace(self.wl, steps=[st])
+        plan, pages, tokens = self.kvx.device_plan(st.reqs, self.S.T, self.D.T)
+        self.subset = (self.kvx.device_reqs(st.reqs), plan, pages, tokens, run_oracle(wl, self.init)[0]["B"])
 
     def call(self, check=True):
         """One planned call into a fresh copy of the destination; returns the
         launch it took."""
         import torch
+        reqs, plan, pages, tokens, want = self.subset or (self.reqs, self.plan, self.pages, self.tokens,
+                                                          self.want)
         self.b.copy_(self.b0)
         self.err.zero_()
-        self.kvx.kvx_transfer_planned(self.a, self.S, self.b, self.D, self.spt, self.dpt, self.reqs,
-                                      self.plan, self.pages, self.tokens, None, self.err)
+        self.kvx.kvx_transfer_planned(self.a, self.S, self.b, self.D, self.spt, self.dpt, reqs, plan, pages,
+                                      tokens, None, self.err)
         launch = self.kvx.kvx_last_launch()
         if check:
             torch.cuda.synchronize()
             assert int(self.err.item()) == 0
-            assert np.array_equal(self.b.cpu().numpy(), self.want)
+            assert np.array_equal(self.b.cpu().numpy(), want)
         return launch
 
 
@@ -106,6 +123,27 @@ def test_keys_are_separate_and_setting_the_mode_starts_over(kvx):
     assert c1.call() in (S, G)
     kvx.kvx_set_launch_choice(kvx.CHOOSE_MEASURED)           # forgets every key
     assert [c1.call() for _ in range(10)] == MEASURE
+
+
+def test_other_records_on_the_same_pools_share_the_measurement(kvx):
+    """A serving loop moves other requests in every call: calls on the same
+    pools count toward one measurement whatever their records, and keep its
+    decision."""
+    import torch
+    c = Case(kvx, seed=61)
+    S, G = kvx.LAUNCH_SWEEP, kvx.LAUNCH_GRID
+    rows = c.st.reqs.tolist()
+    launches = []
+    for i in range(10):
+        c.use_records(rows[: 1 + i % 3] if i % 2 else None)   # the full set, or its first 1-3 records
+        launches.append(c.call())
+    assert launches == MEASURE
+    torch.cuda.synchronize()
+    c.use_records(rows[:2])
+    decided = c.call()
+    assert decided in (S, G)
+    c.use_records(None)
+    assert [c.call() for _ in range(3)] == [decided] * 3
 
 
 @pytest.mark.parametrize("mode,launch", [("CHOOSE_SWEEP", "LAUNCH_SWEEP"), ("CHOOSE_GRID", "LAUNCH_GRID")])
