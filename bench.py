@@ -200,7 +200,7 @@ def summary(r: dict) -> dict:
          "sample_bit_exact": r["sample_bit_exact"], "sample_layers": r["sample_layers"]}
     for k in ("per_step_kernel_ms", "per_step_kernel_ms_median", "per_step_kernel_ms_min",
               "hip_memcpy_d2d_GBps_read_plus_write", "hip_memcpy_d2h_GBps",
-              "hip_memcpy_h2d_GBps", "per_op"):
+              "hip_memcpy_h2d_GBps", "per_op", "both_launches_GBps"):
         if k in c:
             s[k] = c[k]
     return s
@@ -450,6 +450,33 @@ def measure(name: str, args, cpu_layers: int, time_cpu: bool):
             e1.record(stream)
             torch.cuda.synchronize()
             context[key] = round(nb / (e0.elapsed_time(e1) / 1e3) / 1e9, 2)
+
+    if any(d.get("plan") is not None and not d["st"].layer_group for d in dsteps) and len(dsteps) == 1:
+        # after everything else: both launches fixed in turn on the same pools,
+        # to show what the launch kept for the timed steps was chosen from
+        d = dsteps[0]
+        mode = kvx.kvx_launch_choice()
+        rates = {}
+        try:
+            for key, fixed in (("sweep", kvx.CHOOSE_SWEEP), ("grid", kvx.CHOOSE_GRID)):
+                kvx.kvx_set_launch_choice(fixed)
+                launch_step(kvx, wl, mem, d, errw)
+                if kvx.kvx_last_launch() != {"sweep": kvx.LAUNCH_SWEEP, "grid": kvx.LAUNCH_GRID}[key]:
+                    continue                     # this step cannot take that launch
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(4):
+                    launch_step(kvx, wl, mem, d, errw)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                rates[key] = round(dom_bytes / (e0.elapsed_time(e1) / 4 / 1e3) / 1e9, 1)
+        finally:
+            kvx.kvx_set_launch_choice(mode)
+        if int(errw.item()):
+            log(f"device error bits {int(errw.item())}")
+            return None
+        context["both_launches_GBps"] = rates
+        log(f"both launches, fixed, after the run: {rates}")
 
     n_tok = sum(st.n_tokens for st in wl.steps)
     config = {"workload": wl.title, "name": name,
